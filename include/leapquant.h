@@ -1,0 +1,195 @@
+/*
+ * leapquant.h -- C ABI of the LeapQuant 8-bit recurrent-state decode path for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * LeapQuant (arXiv 2609.38166) keeps the recurrent state of a gated delta-rule
+ * linear-attention head (GDN: scalar decay, KDA: per-key-channel decay) in 8
+ * bits.  Within a window of W tokens the quantized state is held fixed and the
+ * tokens' rank-one updates are buffered in FP16 (Sec. 3.2); outputs are read
+ * from the fixed state plus the buffer (App. B.2-B.3).  At the window end the
+ * state is reconstructed, its largest structure is refitted as r FP16
+ * "Compensator Tokens" (Sec. 3.3), the rest is smoothed across key channels
+ * (Sec. 3.4) and re-quantized per value channel (App. B.3).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - One tile = one (request b, value head h) pair; tiles are numbered
+ *    b * heads_v + h.  d_k = d_v = 128 in this version.
+ *  - Every array argument is a caller-owned DEVICE pointer, dense, row-major,
+ *    16-byte aligned.  The library allocates no memory, keeps no global state
+ *    and never synchronises (except leapquant_check_error).  Work is enqueued on
+ *    `stream` (a hipStream_t; NULL = the default stream) and returns at once.
+ *    Calls on different streams with disjoint buffers may run concurrently.
+ *  - The state of one tile is stored TRANSPOSED (value-major): row v holds the
+ *    d_k key-channel entries of value channel v, S^T[v][k].
+ *  - Status codes: LQ_OK (0) or a negative LQ_E* value.  Arguments are
+ *    validated on the host before anything is enqueued; a failed validation
+ *    enqueues nothing.  Data values are not checked: non-finite inputs give
+ *    unspecified (but memory-safe) results.
+ *  - Misuse only the device can see (a decode step on a tile whose window
+ *    buffer is already full) sets a bit in the sticky word *err, writes NaN to
+ *    that tile's output and leaves the tile's state untouched;
+ *    leapquant_check_error() reports and clears it.
+ */
+#ifndef LEAPQUANT_H
+#define LEAPQUANT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---- */
+#define LQ_OK            0
+#define LQ_EINVAL       -1   /* NULL pointer, non-positive size, inconsistent heads   */
+#define LQ_EALIGN       -2   /* a pointer is not 16-byte aligned                      */
+#define LQ_EUNSUPPORTED -3   /* d_k/d_v != 128, r > 16, W out of range, ...           */
+#define LQ_EHIP         -4   /* a HIP call failed (kernel launch, synchronisation)    */
+#define LQ_EDEVICE      -5   /* a sticky device error was found by check_error        */
+
+/* ---- enumerations ---- */
+#define LQ_GATE_SCALAR 0     /* GDN: D_t = alpha_t I                 (App. A table)   */
+#define LQ_GATE_DIAG   1     /* KDA: D_t = Diag(alpha_t), alpha_t in R^{d_k}          */
+#define LQ_CODE_INT8   0     /* symmetric INT8, dequant = code * delta_v, |code|<=127 */
+#define LQ_CODE_E4M3   1     /* OCP FP8 E4M3FN codes, dequant = e4m3(code) * delta_v  */
+#define LQ_STATE_F32   0     /* baseline state in fp32                               */
+#define LQ_STATE_BF16  1     /* baseline state in bf16, rounded to nearest even      */
+
+/* bits of the sticky device error word */
+#define LQ_DEVERR_WINDOW_FULL 1   /* decode_step on a tile with rec_len == window      */
+#define LQ_DEVERR_BAD_REC_LEN 2   /* a tile's rec_len is outside [0, window]; untouched */
+
+/* Limits of this version. */
+#define LQ_MAX_COMP        16
+#define LQ_MAX_WINDOW_GDN 256
+#define LQ_MAX_WINDOW_KDA  64
+#define LQ_MAX_POWER_ITERS 64
+
+/* Shape and method parameters (host struct, read at each call). */
+typedef struct {
+    int32_t batch;       /* B, requests                                              */
+    int32_t heads_v;     /* value heads per request; tiles = batch * heads_v         */
+    int32_t heads_k;     /* key heads; value head h reads key head h / (heads_v/heads_k) */
+    int32_t d_k, d_v;    /* head dimensions (128, 128)                               */
+    int32_t window;      /* W >= 1: tokens buffered before the state is re-quantized */
+    int32_t n_comp;      /* r in [0, 16]: Compensator Tokens per tile                */
+    int32_t power_iters; /* power-iteration sweeps per token, >= 1 when r > 0        */
+    int32_t gate;        /* LQ_GATE_SCALAR or LQ_GATE_DIAG                            */
+    int32_t code;        /* LQ_CODE_INT8 or LQ_CODE_E4M3                             */
+    int32_t smooth;      /* 1: residual smoothing (Sec. 3.4); 0: c = 1               */
+} lq_dims;
+
+/* The quantized state of all tiles (device pointers, caller-owned).
+ * Sizes per tile; g = 1 for the scalar gate, g = d_k for the diagonal gate. */
+typedef struct {
+    void     *codes;   /* [d_v][d_k] bytes: int8 two's complement or E4M3FN        */
+    float    *scale;   /* [d_v]  delta_v = max_k |R^C_kv| / 127 (INT8) or / 448    */
+    float    *smooth;  /* [d_k]  c_k, the residual smoothing scale                 */
+    uint16_t *comp_k;  /* [r][d_k] fp16 key vectors k~_h of the Compensator Tokens */
+    uint16_t *comp_u;  /* [r][d_v] fp16 value vectors u~_h                          */
+    uint16_t *rec_k;   /* [W][d_k] fp16 buffered write keys  k~_j = beta_j k_j      */
+    uint16_t *rec_u;   /* [W][d_v] fp16 buffered corrections u_j                    */
+    uint16_t *rec_a;   /* [W][g]   fp16 buffered decays alpha_j                     */
+    int32_t  *rec_len; /* [1] per tile: records in the open window (0..W)           */
+    int32_t  *err;     /* [1] sticky device error word (LQ_DEVERR_* bits); required */
+} lq_state;
+
+/*
+ * leapquant_state_bytes -- host only, no device access.
+ * Byte sizes of the ten lq_state buffers for all tiles, in field order
+ * (codes, scale, smooth, comp_k, comp_u, rec_k, rec_u, rec_a, rec_len, err).
+ * With r = 4, d = 128 the window-boundary representation (codes, scale,
+ * smooth, comp_k, comp_u) is 1.1875 bytes per state element (Sec. 4.3,
+ * "Memory reduction").
+ */
+int32_t leapquant_state_bytes(const lq_dims *dims, size_t bytes_out[10]);
+
+/*
+ * leapquant_quantize_state -- quantize given fp32 states (a prefill result or a
+ * prefix-cache snapshot) into the window-start representation and open an
+ * empty window.  Sec. 3.3 Eq. (compensator-rank-r), Sec. 3.4, App. B.3.
+ *   S   [B][heads_v][d_v][d_k] fp32, S^T of every tile; read only.
+ *   st  codes, scale, smooth, comp_k, comp_u written; rec_len set to 0.
+ * The r tokens are fitted one after another by power iteration on the
+ * deflated residual, starting each from the residual's key-row l2 norms; each
+ * token is rounded to FP16 before it is subtracted, so the codes absorb that
+ * rounding.  c_k = sqrt(max(mean_v |R_kv|, 1e-12)), R^C = R * (1/c_k),
+ * delta_v = max_k |R^C_kv| / 127, code = clamp(rint(R^C * 127/max), +-127).
+ */
+int32_t leapquant_quantize_state(const lq_dims *dims, const float *S, lq_state *st, void *stream);
+
+/*
+ * leapquant_decode_step -- one token for every tile.  Sec. 3.2 Eq. (record),
+ * App. B.2 Eq. (readout), App. B.3 Eq. (smooth-readout).
+ *   q, k   [B][heads_k][d_k] fp32      v [B][heads_v][d_v] fp32
+ *   alpha  [B][heads_v] (scalar gate) or [B][heads_v][d_k] (diagonal gate) fp32
+ *   beta   [B][heads_v] fp32           o [B][heads_v][d_v] fp32 (written)
+ * With i = rec_len + 1 and the token's decay rounded to FP16:
+ *   A^T x = delta . (Z^T (c . Gamma_{1:i} x)) + U~ (K~^T Gamma_{1:i} x)
+ *           + sum_{j<i} u_j (k~_j^T Gamma_{j+1:i} x)          for x = k, q
+ *   u_i = fp16(v - A^T k),  k~_i = fp16(beta k),  o = A^T q + u_i (k~_i . q)
+ * and the record (alpha_i, k~_i, u_i) is appended; rec_len += 1.  A tile whose
+ * rec_len already equals W is not modified: its o is NaN and
+ * LQ_DEVERR_WINDOW_FULL is raised in *err.
+ */
+int32_t leapquant_decode_step(const lq_dims *dims, lq_state *st, const float *q, const float *k,
+                              const float *v, const float *alpha, const float *beta, float *o,
+                              void *stream);
+
+/*
+ * leapquant_window_commit -- end the window of the selected tiles.  Sec. 3.3
+ * (refit at the window end), Sec. 3.4 Eq. (smooth).
+ *   mask  [B] int32 on the device, nonzero = commit every head of request b;
+ *         NULL = commit all requests.
+ * For a selected tile with p = rec_len > 0 records, reconstruct
+ *   S_p = Gamma_{1:p} [C dequant(Z) + K~ U~^T] + sum_j Gamma_{j+1:p} k~_j u_j^T
+ * in fp32, discard the old tokens, re-quantize S_p exactly as
+ * leapquant_quantize_state does and set rec_len = 0.  A partial window
+ * (p < W) is legal; tiles with rec_len == 0 or an unselected request are left
+ * untouched.
+ */
+int32_t leapquant_window_commit(const lq_dims *dims, lq_state *st, const int32_t *mask,
+                                void *stream);
+
+/*
+ * leapquant_baseline_step -- one token of the unquantized recurrence with a
+ * dense state, the per-step baseline of Sec. 4.1.  Sec. 3.1 Eq. (general):
+ *   A = D S,  u = v - A^T k,  S = A + (beta k) u^T,  o = S^T q,
+ * state S [B][heads_v][d_v][d_k] updated in place, fp32 (LQ_STATE_F32) or
+ * bf16 bits (LQ_STATE_BF16, rounded to nearest even after the step).
+ * Arithmetic is fp32.  Other arguments as leapquant_decode_step (the decay is
+ * not rounded).
+ */
+int32_t leapquant_baseline_step(const lq_dims *dims, void *S, int32_t state_dtype,
+                                const float *q, const float *k, const float *v,
+                                const float *alpha, const float *beta, float *o, void *stream);
+
+/*
+ * leapquant_dequantize_state -- materialise the current fp32 state of every
+ * tile, base plus the rec_len buffered records (Sec. 3.2 Eq. (window) with
+ * Sec. 3.4 Eq. (smooth)), into S_out [B][heads_v][d_v][d_k] (S^T).  Read only
+ * on st.  For inspection, checkpoint export and tests.
+ */
+int32_t leapquant_dequantize_state(const lq_dims *dims, const lq_state *st, float *S_out,
+                                   void *stream);
+
+/*
+ * leapquant_check_error -- synchronise `stream`, copy the sticky word *err to
+ * *bits_out (may be NULL), clear it, and return LQ_EDEVICE if any bit was set,
+ * LQ_OK otherwise (LQ_EHIP if synchronisation failed).
+ */
+int32_t leapquant_check_error(const lq_state *st, void *stream, int32_t *bits_out);
+
+/* Static description of a status code. */
+const char *leapquant_strerror(int32_t status);
+
+/* Text of the last HIP error seen by this thread in a failing call, or "". */
+const char *leapquant_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LEAPQUANT_H */

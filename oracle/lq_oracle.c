@@ -460,7 +460,20 @@ typedef struct {
     double *rec_k;     /* [tiles][W][dk] */
     double *rec_u;     /* [tiles][W][dv] */
     int32_t *rec_len;  /* [tiles] */
+    double *hist_a;    /* [tiles][T][g] every token's record (may be NULL) */
+    double *hist_k;    /* [tiles][T][dk] */
+    double *hist_u;    /* [tiles][T][dv] */
 } lqo_outputs;
+
+static void store_hist(const lqo_cfg *cfg, const lqo_outputs *out, size_t ts, const double *ra,
+                       const double *rk, const double *ru)
+{
+    if (!out->hist_a) return;
+    const int dk = cfg->dk, dv = cfg->dv, g = cfg->gate ? dk : 1;
+    memcpy(out->hist_a + ts * g, ra, sizeof(double) * g);
+    memcpy(out->hist_k + ts * dk, rk, sizeof(double) * dk);
+    memcpy(out->hist_u + ts * dv, ru, sizeof(double) * dv);
+}
 
 typedef struct {
     const float *q;     /* [tiles][T][dk] */
@@ -527,6 +540,7 @@ int OQ(run_dense)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
             window_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, in->v + ts * dv,
                              in->alpha + ts * g, in->beta[ts], o + ts * dv, ra + (size_t)n * g,
                              rk + (size_t)n * dk, ru + (size_t)n * dv, u);
+            store_hist(cfg, out, ts, ra + (size_t)n * g, rk + (size_t)n * dk, ru + (size_t)n * dv);
             if (++n == W) {
                 if (cfg->quantize) {
                     for (int i = 0; i < dk * dv; ++i) Sd[i] = (double)S[i];
@@ -588,6 +602,7 @@ int OQ(run_readout)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
                              in->q + ts * dk, in->k + ts * dk, in->v + ts * dv, in->alpha + ts * g,
                              in->beta[ts], o + ts * dv, ra + (size_t)n * g, rk + (size_t)n * dk,
                              ru + (size_t)n * dv);
+            store_hist(cfg, out, ts, ra + (size_t)n * g, rk + (size_t)n * dk, ru + (size_t)n * dv);
             if (++n == W) {
                 OQ(reconstruct)(cfg, cfg->quantize ? Z : NULL, delta, c, Kt, Ut, Sd, ra, rk, ru, n, Sd);
                 if (cfg->quantize) {

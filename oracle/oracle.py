@@ -45,7 +45,8 @@ class _Inputs(C.Structure):
 
 class _Outputs(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in (
-        "Z", "delta", "c", "Kt", "Ut", "S_final", "rec_a", "rec_k", "rec_u", "rec_len")]
+        "Z", "delta", "c", "Kt", "Ut", "S_final", "rec_a", "rec_k", "rec_u", "rec_len", "hist_a",
+        "hist_k", "hist_u")]
 
 
 GATE_SCALAR, GATE_DIAG = 0, 1
@@ -236,7 +237,8 @@ def _inputs(tok: dict, tiles: int, T: int, cfg: Cfg):
     return st, arrs
 
 
-def _run_window(name, cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None, prec=64):
+def _run_window(name, cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None, prec=64,
+                history=False):
     S_init = np.ascontiguousarray(S_init, dtype=np.float64)
     tiles = S_init.shape[0]
     T = np.asarray(tok["q"]).shape[1]
@@ -253,8 +255,12 @@ def _run_window(name, cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None,
                     "delta": np.zeros((tiles, ns, cfg.dv), np.float32),
                     "c": np.zeros((tiles, ns, cfg.dk), np.float32),
                     "Kt": np.zeros((tiles, ns, r, cfg.dk)), "Ut": np.zeros((tiles, ns, r, cfg.dv))})
+    if history:
+        res.update({"hist_a": np.zeros((tiles, T, g)), "hist_k": np.zeros((tiles, T, cfg.dk)),
+                    "hist_u": np.zeros((tiles, T, cfg.dv))})
     out = _Outputs(*[_p(res.get(n)) for n in ("Z", "delta", "c", "Kt", "Ut", "S_final", "rec_a",
-                                             "rec_k", "rec_u", "rec_len")])
+                                             "rec_k", "rec_u", "rec_len", "hist_a", "hist_k",
+                                             "hist_u")])
     _fn(name, prec)(C.byref(cfg), tiles, T, _p(S_init), C.byref(st), _p(res["o"]), C.byref(out),
                     threads or default_threads())
     if snapshots:
@@ -264,14 +270,16 @@ def _run_window(name, cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None,
     return res
 
 
-def run_dense(cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None, prec=64) -> dict:
+def run_dense(cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None, prec=64,
+              history=False) -> dict:
     """Per-window method in dense form over [tiles] independent tiles."""
-    return _run_window("run_dense", cfg, S_init, tok, snapshots, threads, prec)
+    return _run_window("run_dense", cfg, S_init, tok, snapshots, threads, prec, history)
 
 
-def run_readout(cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None, prec=64) -> dict:
+def run_readout(cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None, prec=64,
+                history=False) -> dict:
     """Per-window method in readout form (the structure a decode kernel follows)."""
-    return _run_window("run_readout", cfg, S_init, tok, snapshots, threads, prec)
+    return _run_window("run_readout", cfg, S_init, tok, snapshots, threads, prec, history)
 
 
 def run_baseline(cfg: Cfg, S_init, tok: dict, mode=STATE_F32, threads=None, prec=64,

@@ -1,0 +1,155 @@
+// Per-step baseline with a dense fp32 or bf16 state (Sec. 4.1 "Baselines"):
+//   A = D S,  u = v - A^T k,  S = A + (beta k) u^T,  o = S^T q   (Sec. 3.1)
+// One 256-thread workgroup per tile; 16 lanes cover one 128-entry state row
+// S^T[v][:] (8 key channels each), so both matvecs are DPP row reductions.
+// The state is read once and written once; arithmetic is fp32, a bf16 state is
+// rounded to nearest even after the update and the output reads the rounded
+// state.
+#include "lq_device.hpp"
+#include "lq_internal.hpp"
+
+namespace lq {
+
+namespace {
+
+struct BaseArgs {
+    void *S;
+    const float *q;
+    const float *k;
+    const float *v;
+    const float *alpha;
+    const float *beta;
+    float *o;
+    int heads_v;
+    int group;
+};
+
+template <int GATE, int BF16>
+__global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
+    const int tile = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int l16 = tid & 15;
+    const int r0 = tid >> 4;                  // rows r0 + 16 m
+    const int b = tile / a.heads_v, hv = tile - b * a.heads_v;
+    const size_t kvec = ((size_t)b * (a.heads_v / a.group) + hv / a.group) * D + 8 * l16;
+    const size_t tvec = (size_t)tile * D;
+
+    float kx[8], qx[8], al[8], bk[8];
+    const float4 *k4 = (const float4 *)(a.k + kvec);
+    const float4 *q4 = (const float4 *)(a.q + kvec);
+    {
+        const float4 k0 = k4[0], k1 = k4[1], q0 = q4[0], q1 = q4[1];
+        kx[0] = k0.x; kx[1] = k0.y; kx[2] = k0.z; kx[3] = k0.w;
+        kx[4] = k1.x; kx[5] = k1.y; kx[6] = k1.z; kx[7] = k1.w;
+        qx[0] = q0.x; qx[1] = q0.y; qx[2] = q0.z; qx[3] = q0.w;
+        qx[4] = q1.x; qx[5] = q1.y; qx[6] = q1.z; qx[7] = q1.w;
+    }
+    if (GATE) {
+        const float4 *a4 = (const float4 *)(a.alpha + tvec + 8 * l16);
+        const float4 a0 = a4[0], a1 = a4[1];
+        al[0] = a0.x; al[1] = a0.y; al[2] = a0.z; al[3] = a0.w;
+        al[4] = a1.x; al[5] = a1.y; al[6] = a1.z; al[7] = a1.w;
+    } else {
+        const float s = a.alpha[tile];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) al[j] = s;
+    }
+    const float beta = a.beta[tile];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) bk[j] = beta * kx[j];
+
+    float s[8][8];
+    if (BF16) {
+        const uint16_t *St = (const uint16_t *)a.S + (size_t)tile * D * D;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const uint4 p = *(const uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
+            const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                s[m][2 * i] = bf2f((uint16_t)(w[i] & 0xFFFFu));
+                s[m][2 * i + 1] = bf2f((uint16_t)(w[i] >> 16));
+            }
+        }
+    } else {
+        const float *St = (const float *)a.S + (size_t)tile * D * D;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const float4 *row = (const float4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
+            const float4 lo = row[0], hi = row[1];
+            s[m][0] = lo.x; s[m][1] = lo.y; s[m][2] = lo.z; s[m][3] = lo.w;
+            s[m][4] = hi.x; s[m][5] = hi.y; s[m][6] = hi.z; s[m][7] = hi.w;
+        }
+    }
+
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        const int vrow = r0 + 16 * m;
+        float p = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            s[m][j] *= al[j];                           // A = D S
+            p = fmaf(s[m][j], kx[j], p);
+        }
+        const float u = a.v[tvec + vrow] - row16_sum(p);  // u = v - A^T k
+        float po = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float x = fmaf(bk[j], u, s[m][j]);          // S = A + (beta k) u^T
+            if (BF16) x = bf2f(f2bf(x));
+            s[m][j] = x;
+            po = fmaf(x, qx[j], po);
+        }
+        po = row16_sum(po);
+        if (l16 == 0) a.o[tvec + vrow] = po;             // o = S^T q
+    }
+
+    if (BF16) {
+        uint16_t *St = (uint16_t *)a.S + (size_t)tile * D * D;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            uint4 w;
+            w.x = f2bf(s[m][0]) | ((uint32_t)f2bf(s[m][1]) << 16);
+            w.y = f2bf(s[m][2]) | ((uint32_t)f2bf(s[m][3]) << 16);
+            w.z = f2bf(s[m][4]) | ((uint32_t)f2bf(s[m][5]) << 16);
+            w.w = f2bf(s[m][6]) | ((uint32_t)f2bf(s[m][7]) << 16);
+            *(uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16) = w;
+        }
+    } else {
+        float *St = (float *)a.S + (size_t)tile * D * D;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            float4 *row = (float4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
+            row[0] = make_float4(s[m][0], s[m][1], s[m][2], s[m][3]);
+            row[1] = make_float4(s[m][4], s[m][5], s[m][6], s[m][7]);
+        }
+    }
+}
+
+template <int GATE, int BF16>
+hipError_t launch(const BaseArgs &a, int tiles, hipStream_t st) {
+    hipLaunchKernelGGL((baseline_kernel<GATE, BF16>), dim3(tiles), dim3(NT), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_baseline(const lq_dims &d, void *S, int state_dtype, const TokenPtrs &t,
+                           hipStream_t st) {
+    BaseArgs a;
+    a.S = S;
+    a.q = t.q;
+    a.k = t.k;
+    a.v = t.v;
+    a.alpha = t.alpha;
+    a.beta = t.beta;
+    a.o = t.o;
+    a.heads_v = d.heads_v;
+    a.group = d.heads_v / d.heads_k;
+    const int tiles = d.batch * d.heads_v;
+    const bool bf = state_dtype == LQ_STATE_BF16;
+    if (d.gate == LQ_GATE_DIAG) return bf ? launch<1, 1>(a, tiles, st) : launch<1, 0>(a, tiles, st);
+    return bf ? launch<0, 1>(a, tiles, st) : launch<0, 0>(a, tiles, st);
+}
+
+}  // namespace lq

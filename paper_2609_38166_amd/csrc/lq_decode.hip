@@ -1,0 +1,289 @@
+// Decode step: one token for every (request, head) tile.
+//
+// One 256-thread workgroup owns one tile.  With i = rec_len + 1 it reads
+//   A_i^T x = delta . (Z^T (c . Gamma_{1:i} x))            quantized residual
+//           + U~ (K~^T (Gamma_{1:i} x))                     Compensator Tokens
+//           + sum_{j<i} u_j (k~_j^T (Gamma_{j+1:i} x))      buffered records
+// for x = k_t and x = q_t in one pass over the codes (App. B.2 Eq. (readout),
+// App. B.3 Eq. (smooth-readout)), then forms u_t = fp16(v_t - A^T k_t), the
+// output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
+// appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
+//
+// Memory traffic per tile: the d_v x d_k code bytes once (16-byte loads, 8
+// lanes per 128-byte row, coalesced), scales and smoothing, r token pairs, the
+// i-1 buffered records, the token's inputs, one record and the output written.
+// The decays Gamma are products of the FP16 record decays, formed on the fly
+// from the newest record backwards, so no d_k x d_v intermediate exists.
+#include "lq_device.hpp"
+#include "lq_internal.hpp"
+
+namespace lq {
+
+namespace {
+
+constexpr int CHUNK = 16;   // records per pass: one 16-lane group per record
+
+struct DecodeArgs {
+    const uint8_t *codes;
+    const float *scale;
+    const float *smooth;
+    const uint16_t *comp_k;
+    const uint16_t *comp_u;
+    uint16_t *rec_k;
+    uint16_t *rec_u;
+    uint16_t *rec_a;
+    int32_t *rec_len;
+    int32_t *err;
+    const float *q;
+    const float *k;
+    const float *v;
+    const float *alpha;
+    const float *beta;
+    float *o;
+    int heads_v;
+    int group;      // heads_v / heads_k
+    int window;
+    int n_comp;
+};
+
+template <int GATE, int CODE>
+__global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
+    constexpr int G = GATE ? D : 1;     // decay values per record
+    __shared__ float s_x[2][D];          // x = k_t, q_t
+    __shared__ float s_w[2][D];          // c . Gamma_{1:i} . x
+    __shared__ float s_y[2][D];          // Gamma_{1:i} . x
+    __shared__ float s_z[2][D];          // quantized-residual readout
+    __shared__ float s_P[CHUNK][G];      // Gamma_{j+1:i} of the records in this pass
+    __shared__ float s_red[CHUNK][2][D]; // per-group partial readouts
+    __shared__ float s_kq[2];            // k~_t . q_t (per wave pair)
+
+    const int tile = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int b = tile / a.heads_v, hv = tile - b * a.heads_v;
+    const size_t kvec = ((size_t)b * (a.heads_v / a.group) + hv / a.group) * D;
+    const size_t tvec = (size_t)tile * D;
+
+    const int n = a.rec_len[tile];
+    if (n >= a.window || n < 0) {        // window buffer full (or corrupt): tile untouched
+        if (tid == 0) atomicOr(a.err, n < 0 ? (int)LQ_DEVERR_BAD_REC_LEN : (int)LQ_DEVERR_WINDOW_FULL);
+        if (tid < D) a.o[tvec + tid] = __builtin_nanf("");
+        return;
+    }
+
+    // ---- issue the code loads first: 4 rows x 16 bytes per thread --------------
+    const int g8 = tid & 7;              // 16-channel key segment
+    const int rg = tid >> 3;             // rows rg, rg+32, rg+64, rg+96
+    const uint8_t *zt = a.codes + (size_t)tile * D * D;
+    uint4 zr[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) zr[m] = *(const uint4 *)(zt + (size_t)(rg + 32 * m) * D + 16 * g8);
+
+    // ---- token inputs, this token's record -------------------------------------
+    float carry = 1.0f;                  // running Gamma_{j+1:i} (channel tid, or scalar)
+    if (tid < D) {
+        const float kx = a.k[kvec + tid];
+        const float qx = a.q[kvec + tid];
+        s_x[0][tid] = kx;
+        s_x[1][tid] = qx;
+        const float al = GATE ? a.alpha[tvec + tid] : a.alpha[tile];
+        const uint16_t ah = f2h(al);
+        carry = h2f(ah);
+        const size_t slot = (size_t)tile * a.window + n;
+        if (GATE) a.rec_a[slot * D + tid] = ah;
+        else if (tid == 0) a.rec_a[slot] = ah;
+        const uint16_t tkh = f2h(a.beta[tile] * kx);         // k~_t = fp16(beta_t k_t)
+        a.rec_k[slot * D + tid] = tkh;
+        float kq = wave_sum(h2f(tkh) * qx);
+        if ((tid & 63) == 0) s_kq[tid >> 6] = kq;
+    }
+    __syncthreads();
+
+    // ---- buffered records, newest first, CHUNK per pass -------------------------
+    const int l16 = tid & 15;            // 8-channel key segment / 8-value segment
+    const int ts = tid >> 4;             // term slot 0..15
+    float xk[8], xq[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        xk[j] = s_x[0][8 * l16 + j];
+        xq[j] = s_x[1][8 * l16 + j];
+    }
+    float acc_k[8], acc_q[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc_k[j] = acc_q[j] = 0.0f;
+
+    const size_t rbase = (size_t)tile * a.window;
+    for (int hi = n; hi > 0; hi -= CHUNK) {
+        const int lo = hi > CHUNK ? hi - CHUNK : 0;
+        // suffix decays of records lo..hi-1: P_r = prod of alpha over records r+1..n-1 and token i
+        if (tid < D) {
+            for (int r = hi - 1; r >= lo; --r) {
+                if (GATE) {
+                    s_P[r - lo][tid] = carry;
+                    carry *= h2f(a.rec_a[(rbase + r) * D + tid]);
+                } else {
+                    if (tid == 0) s_P[r - lo][0] = carry;
+                    carry *= h2f(a.rec_a[rbase + r]);
+                }
+            }
+        }
+        __syncthreads();
+        const int r = lo + ts;
+        if (r < hi) {
+            const uint4 kp = *(const uint4 *)(a.rec_k + (rbase + r) * D + 8 * l16);
+            const uint4 up = *(const uint4 *)(a.rec_u + (rbase + r) * D + 8 * l16);
+            float kv[8], uv[8];
+            unpack_h8(kp, kv);
+            unpack_h8(up, uv);
+            float pk = 0.0f, pq = 0.0f;
+            if (GATE) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float t = kv[j] * s_P[ts][(8 * l16 + j) % G];
+                    pk = fmaf(t, xk[j], pk);
+                    pq = fmaf(t, xq[j], pq);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    pk = fmaf(kv[j], xk[j], pk);
+                    pq = fmaf(kv[j], xq[j], pq);
+                }
+            }
+            pk = row16_sum(pk);
+            pq = row16_sum(pq);
+            if (!GATE) {
+                const float p = s_P[ts][0];
+                pk *= p;
+                pq *= p;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
+                acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- carry is now Gamma_{1:i}: base and token read vectors -------------------
+    if (tid < D) {
+        const float c = a.smooth[tvec + tid];
+        const float gm = carry;      // scalar gate: every thread < D carries the same product
+        const float yk = gm * s_x[0][tid], yq = gm * s_x[1][tid];
+        s_y[0][tid] = yk;
+        s_y[1][tid] = yq;
+        s_w[0][tid] = c * yk;
+        s_w[1][tid] = c * yq;
+    }
+    __syncthreads();
+
+    // ---- quantized residual: rows rg + 32m, channels 16*g8 .. +15 ---------------
+    {
+        float wk[16], wq[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            wk[j] = s_w[0][16 * g8 + j];
+            wq[j] = s_w[1][16 * g8 + j];
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            float f[16];
+            decode16<CODE>(zr[m], f);
+            float pk = 0.0f, pq = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                pk = fmaf(f[j], wk[j], pk);
+                pq = fmaf(f[j], wq[j], pq);
+            }
+            pk = row8_sum(pk);
+            pq = row8_sum(pq);
+            if (g8 == 0) {
+                const int vrow = rg + 32 * m;
+                const float dv = a.scale[tvec + vrow];
+                s_z[0][vrow] = dv * pk;
+                s_z[1][vrow] = dv * pq;
+            }
+        }
+    }
+
+    // ---- Compensator Tokens: token ts, same decay as the base -------------------
+    if (ts < a.n_comp) {
+        const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
+        const uint4 kp = *(const uint4 *)(a.comp_k + cb);
+        const uint4 up = *(const uint4 *)(a.comp_u + cb);
+        float kv[8], uv[8];
+        unpack_h8(kp, kv);
+        unpack_h8(up, uv);
+        float pk = 0.0f, pq = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            pk = fmaf(kv[j], s_y[0][8 * l16 + j], pk);
+            pq = fmaf(kv[j], s_y[1][8 * l16 + j], pq);
+        }
+        pk = row16_sum(pk);
+        pq = row16_sum(pq);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
+            acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        s_red[ts][0][8 * l16 + j] = acc_k[j];
+        s_red[ts][1][8 * l16 + j] = acc_q[j];
+    }
+    __syncthreads();
+
+    // ---- combine, correction, output, record ------------------------------------
+    if (tid < D) {
+        float ak = s_z[0][tid], aq = s_z[1][tid];
+#pragma unroll
+        for (int s = 0; s < CHUNK; ++s) {
+            ak += s_red[s][0][tid];
+            aq += s_red[s][1][tid];
+        }
+        const uint16_t uh = f2h(a.v[tvec + tid] - ak);     // u_t = fp16(v_t - A^T k_t)
+        a.rec_u[(rbase + n) * D + tid] = uh;
+        a.o[tvec + tid] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
+        if (tid == 0) a.rec_len[tile] = n + 1;
+    }
+}
+
+template <int GATE, int CODE>
+hipError_t launch(const DecodeArgs &args, int tiles, hipStream_t st) {
+    hipLaunchKernelGGL((decode_kernel<GATE, CODE>), dim3(tiles), dim3(NT), 0, st, args);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &t, hipStream_t st) {
+    DecodeArgs a;
+    a.codes = (const uint8_t *)s.codes;
+    a.scale = s.scale;
+    a.smooth = s.smooth;
+    a.comp_k = s.comp_k;
+    a.comp_u = s.comp_u;
+    a.rec_k = s.rec_k;
+    a.rec_u = s.rec_u;
+    a.rec_a = s.rec_a;
+    a.rec_len = s.rec_len;
+    a.err = s.err;
+    a.q = t.q;
+    a.k = t.k;
+    a.v = t.v;
+    a.alpha = t.alpha;
+    a.beta = t.beta;
+    a.o = t.o;
+    a.heads_v = d.heads_v;
+    a.group = d.heads_v / d.heads_k;
+    a.window = d.window;
+    a.n_comp = d.n_comp;
+    const int tiles = d.batch * d.heads_v;
+    if (d.gate == LQ_GATE_DIAG)
+        return d.code == LQ_CODE_E4M3 ? launch<1, 1>(a, tiles, st) : launch<1, 0>(a, tiles, st);
+    return d.code == LQ_CODE_E4M3 ? launch<0, 1>(a, tiles, st) : launch<0, 0>(a, tiles, st);
+}
+
+}  // namespace lq

@@ -1,0 +1,401 @@
+// Whole-tile kernels: quantize a given state, commit a window, dequantize.
+//
+// One 256-thread workgroup owns one 128 x 128 tile held in registers: thread
+// (kb, vb) keeps the 8 x 8 block M[8kb .. 8kb+7][8vb .. 8vb+7] of the state in
+// paper orientation (row = key channel).  kb is the lane's column inside its
+// 16-lane DPP row, so reductions over key channels are DPP row reductions;
+// reductions over value channels go through LDS.
+//
+//   commit   : reconstruct S_p = Gamma_{1:p}[C dequant(Z) + K~ U~^T]
+//              + sum_j Gamma_{j+1:p} k~_j u_j^T  (Sec. 3.4 Eq. (smooth)),
+//              then quantize it and reset the window (Sec. 3.3: the old
+//              tokens are discarded and refitted);
+//   quantize : load a given fp32 state and quantize it;
+//   dequant  : reconstruct and write the fp32 state.
+//
+// Quantization (Sec. 3.3 Eq. (compensator-rank-r), Sec. 3.4, App. B.3): r
+// Compensator Tokens fitted one after another by power iteration on the
+// deflated residual (start: key-row l2 norms; each sweep y = M^T x, x = M y,
+// x *= 1/|x|), each rounded to FP16 before it is subtracted; then the smoothing
+// scales c_k = sqrt(max(mean_v |R_kv|, 1e-12)), the per-value-channel scale
+// delta_v = max_k |R_kv / c_k| / qmax and the codes.
+//
+// Precision: the tile, the fit and the smoothing statistic are carried in
+// fp64 (gfx950 runs fp64 FMA at the rate of unpacked fp32).  Each token is
+// rounded to FP16 before it is deflated, so an fp32-level difference in the
+// fit would flip a rounding and move every later token and the codes of whole
+// rows; in fp64 the discrete decisions (FP16 tokens, fp32 scales, codes) are
+// reproducible by any exact-enough implementation.  The code decision itself
+// is taken in fp32 on the fp32-rounded residual.
+#include "lq_device.hpp"
+#include "lq_internal.hpp"
+
+namespace lq {
+
+namespace {
+
+constexpr int TCH = 16;     // rank-one records staged per pass
+
+struct TileArgs {
+    uint8_t *codes;
+    float *scale;
+    float *smooth;
+    uint16_t *comp_k;
+    uint16_t *comp_u;
+    const uint16_t *rec_k;
+    const uint16_t *rec_u;
+    const uint16_t *rec_a;
+    int32_t *rec_len;
+    int32_t *err;
+    const float *S_in;
+    float *S_out;
+    const int32_t *mask;
+    int heads_v;
+    int window;
+    int n_comp;
+    int power_iters;
+    int smooth_on;
+};
+
+struct TileShared {
+    double part[16][D];     // per-value-block partials of a sum over value channels
+    double vec[D];          // broadcast vector
+    double nrm[2];          // per-wave partial squared norms
+    double key[TCH][D];     // staged record keys, decay folded in
+    float val[TCH][D];      // staged record values
+};
+
+// Sum p[a] (channel 8kb+a, this thread's value block) over the 16 value blocks;
+// thread t < 128 returns the sum for channel t.
+__device__ __forceinline__ double reduce_over_values(TileShared &sh, const double *p, int kb, int vb) {
+#pragma unroll
+    for (int a = 0; a < 8; ++a) sh.part[vb][8 * kb + a] = p[a];
+    __syncthreads();
+    double s = 0.0;
+    const int t = threadIdx.x;
+    if (t < D) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s += sh.part[j][t];
+    }
+    return s;
+}
+
+// Threads t < 128 publish x (channel t); after the barrier every thread reads
+// its 8 channels into xa and gets the squared norm of the whole vector.  The
+// barrier also ends every read of sh.part issued before the call.
+__device__ __forceinline__ double publish_vector(TileShared &sh, double x, double *xa, int kb) {
+    const int t = threadIdx.x;
+    if (t < D) {
+        sh.vec[t] = x;
+        const double s = wave_sum(x * x);
+        if ((t & 63) == 0) sh.nrm[t >> 6] = s;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < 8; ++a) xa[a] = sh.vec[8 * kb + a];
+    return sh.nrm[0] + sh.nrm[1];
+}
+
+template <int GATE, int CODE, int MODE>
+__global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
+    __shared__ TileShared sh;
+    const int tile = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int kb = lane & 15;                       // key block  (DPP column)
+    const int vb = (tid >> 6) * 4 + (lane >> 4);    // value block
+    const size_t tvec = (size_t)tile * D;
+    const int r = A.n_comp;
+
+    double m[8][8];                                 // m[a][b] = M[8kb+a][8vb+b]
+
+    if (MODE == TILE_QUANTIZE) {
+        const float *S = A.S_in + (size_t)tile * D * D;
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const float4 *row = (const float4 *)(S + (size_t)(8 * vb + b) * D + 8 * kb);
+            const float4 lo = row[0], hi = row[1];
+            m[0][b] = lo.x; m[1][b] = lo.y; m[2][b] = lo.z; m[3][b] = lo.w;
+            m[4][b] = hi.x; m[5][b] = hi.y; m[6][b] = hi.z; m[7][b] = hi.w;
+        }
+    } else {
+        const int p = A.rec_len[tile];
+        if (p < 0 || p > A.window) {                                  // corrupt: tile untouched
+            if (tid == 0) atomicOr(A.err, (int)LQ_DEVERR_BAD_REC_LEN);
+            return;
+        }
+        if (MODE == TILE_COMMIT) {
+            const int req = tile / A.heads_v;
+            if (p == 0 || (A.mask && A.mask[req] == 0)) return;   // uniform: tile untouched
+        }
+#pragma unroll
+        for (int a = 0; a < 8; ++a)
+#pragma unroll
+            for (int b = 0; b < 8; ++b) m[a][b] = 0.0;
+
+        // records, newest first: k~_j . Gamma_{j+1:p} staged in LDS, TCH per pass
+        const size_t rbase = (size_t)tile * A.window;
+        double carry = 1.0;                         // running Gamma_{j+1:p}, channel tid
+        for (int hi = p; hi > 0; hi -= TCH) {
+            const int lo = hi > TCH ? hi - TCH : 0;
+            if (tid < D) {
+                for (int j = hi - 1; j >= lo; --j) {
+                    sh.key[j - lo][tid] = carry * (double)h2f(A.rec_k[(rbase + j) * D + tid]);
+                    sh.val[j - lo][tid] = h2f(A.rec_u[(rbase + j) * D + tid]);
+                    carry *= (double)(GATE ? h2f(A.rec_a[(rbase + j) * D + tid])
+                                           : h2f(A.rec_a[rbase + j]));
+                }
+            }
+            __syncthreads();
+            for (int j = 0; j < hi - lo; ++j) {
+                double kv[8], uv[8];
+#pragma unroll
+                for (int a = 0; a < 8; ++a) kv[a] = sh.key[j][8 * kb + a];
+#pragma unroll
+                for (int b = 0; b < 8; ++b) uv[b] = (double)sh.val[j][8 * vb + b];
+#pragma unroll
+                for (int a = 0; a < 8; ++a)
+#pragma unroll
+                    for (int b = 0; b < 8; ++b) m[a][b] = fma(kv[a], uv[b], m[a][b]);
+            }
+            __syncthreads();
+        }
+        // carry = Gamma_{1:p}: decay of the window-start base and its tokens.
+        // Stage the tokens in LDS (r <= TCH); publish_vector's barrier covers it.
+        if (tid < D) {
+            for (int h = 0; h < r; ++h) {
+                sh.key[h][tid] = (double)h2f(A.comp_k[((size_t)tile * r + h) * D + tid]);
+                sh.val[h][tid] = h2f(A.comp_u[((size_t)tile * r + h) * D + tid]);
+            }
+        }
+        double ga[8];
+        publish_vector(sh, carry, ga, kb);
+        double cs[8], dl[8];
+#pragma unroll
+        for (int a = 0; a < 8; ++a) cs[a] = (double)A.smooth[tvec + 8 * kb + a];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) dl[b] = (double)A.scale[tvec + 8 * vb + b];
+        const uint8_t *zt = A.codes + (size_t)tile * D * D;
+        uint2 zp[8];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) zp[b] = *(const uint2 *)(zt + (size_t)(8 * vb + b) * D + 8 * kb);
+        // base + tokens, one key channel at a time so only 8 extra fp64 values are live
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+            double base[8];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                const uint32_t w = a < 4 ? zp[b].x : zp[b].y;
+                const uint32_t z = (w >> (8 * (a & 3))) & 0xFFu;
+                const double zf = CODE ? (double)e4m3_to_f<0>(z) : (double)(int8_t)(uint8_t)z;
+                base[b] = cs[a] * (zf * dl[b]);
+            }
+            for (int h = 0; h < r; ++h) {
+                const double kh = sh.key[h][8 * kb + a];
+#pragma unroll
+                for (int b = 0; b < 8; ++b) base[b] = fma(kh, (double)sh.val[h][8 * vb + b], base[b]);
+            }
+#pragma unroll
+            for (int b = 0; b < 8; ++b) m[a][b] = fma(ga[a], base[b], m[a][b]);
+        }
+
+        if (MODE == TILE_DEQUANT) {
+            float *S = A.S_out + (size_t)tile * D * D;
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                float4 *row = (float4 *)(S + (size_t)(8 * vb + b) * D + 8 * kb);
+                row[0] = make_float4((float)m[0][b], (float)m[1][b], (float)m[2][b], (float)m[3][b]);
+                row[1] = make_float4((float)m[4][b], (float)m[5][b], (float)m[6][b], (float)m[7][b]);
+            }
+            return;
+        }
+        __syncthreads();    // every read of sh.vec above is done before it is reused
+    }
+
+    // ------------------------------------------------------------------ quantize
+    for (int h = 0; h < r; ++h) {
+        double xa[8], p8[8];
+        // start vector: key-row l2 norms of the current residual
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+            double s = 0.0;
+#pragma unroll
+            for (int b = 0; b < 8; ++b) s = fma(m[a][b], m[a][b], s);
+            p8[a] = s;
+        }
+        double x = sqrt(reduce_over_values(sh, p8, kb, vb));
+        double nrm = sqrt(publish_vector(sh, x, xa, kb));
+        bool ok = nrm > 0.0;
+        if (ok) {
+            const double inv = 1.0 / nrm;
+#pragma unroll
+            for (int a = 0; a < 8; ++a) xa[a] *= inv;
+        }
+        for (int it = 0; ok && it < A.power_iters; ++it) {
+            double y[8];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                double s = 0.0;
+#pragma unroll
+                for (int a = 0; a < 8; ++a) s = fma(m[a][b], xa[a], s);
+                y[b] = row16_sum(s);                // y_v = sum_k M_kv x_k
+            }
+#pragma unroll
+            for (int a = 0; a < 8; ++a) {
+                double s = 0.0;
+#pragma unroll
+                for (int b = 0; b < 8; ++b) s = fma(m[a][b], y[b], s);
+                p8[a] = s;
+            }
+            x = reduce_over_values(sh, p8, kb, vb);  // x_k = sum_v M_kv y_v
+            nrm = sqrt(publish_vector(sh, x, xa, kb));
+            if (!(nrm > 0.0)) {
+                ok = false;
+                break;
+            }
+            const double inv = 1.0 / nrm;
+#pragma unroll
+            for (int a = 0; a < 8; ++a) xa[a] *= inv;
+        }
+        uint16_t kh[8], uh[8];
+        if (ok) {
+            double kf[8], uf[8];
+#pragma unroll
+            for (int a = 0; a < 8; ++a) {
+                kh[a] = d2h_via_f32(xa[a]);          // rounded through fp32
+                kf[a] = (double)h2f(kh[a]);
+            }
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                double s = 0.0;
+#pragma unroll
+                for (int a = 0; a < 8; ++a) s = fma(m[a][b], kf[a], s);
+                uh[b] = d2h_via_f32(row16_sum(s));   // u~_v = fp16(sum_k M_kv k~_k)
+                uf[b] = (double)h2f(uh[b]);
+            }
+#pragma unroll
+            for (int a = 0; a < 8; ++a)
+#pragma unroll
+                for (int b = 0; b < 8; ++b) m[a][b] = fma(-kf[a], uf[b], m[a][b]);
+        } else {
+#pragma unroll
+            for (int a = 0; a < 8; ++a) kh[a] = uh[a] = 0;
+        }
+        if (vb == 0) {
+            uint4 w;
+            w.x = kh[0] | ((uint32_t)kh[1] << 16);
+            w.y = kh[2] | ((uint32_t)kh[3] << 16);
+            w.z = kh[4] | ((uint32_t)kh[5] << 16);
+            w.w = kh[6] | ((uint32_t)kh[7] << 16);
+            *(uint4 *)(A.comp_k + ((size_t)tile * r + h) * D + 8 * kb) = w;
+        }
+        if (kb == 0) {
+            uint4 w;
+            w.x = uh[0] | ((uint32_t)uh[1] << 16);
+            w.y = uh[2] | ((uint32_t)uh[3] << 16);
+            w.z = uh[4] | ((uint32_t)uh[5] << 16);
+            w.w = uh[6] | ((uint32_t)uh[7] << 16);
+            *(uint4 *)(A.comp_u + ((size_t)tile * r + h) * D + 8 * vb) = w;
+        }
+    }
+
+    // residual smoothing over key rows: c_k = sqrt(max(mean_v |R_kv|, 1e-12)) in fp32
+    double csd[8];
+    {
+        double p8[8];
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+            double s = 0.0;
+#pragma unroll
+            for (int b = 0; b < 8; ++b) s += fabs(m[a][b]);
+            p8[a] = s;
+        }
+        const double s = reduce_over_values(sh, p8, kb, vb);
+        float c = 1.0f;
+        if (A.smooth_on) c = (float)sqrt(fmax(s * (1.0 / (double)D), (double)1e-12f));
+        if (tid < D) A.smooth[tvec + tid] = c;
+        publish_vector(sh, (double)c, csd, kb);
+    }
+    // per-value-channel scale and codes, decided in fp32
+    constexpr float QMAX = CODE ? 448.0f : 127.0f;
+    float ic[8];
+#pragma unroll
+    for (int a = 0; a < 8; ++a) ic[a] = 1.0f / (float)csd[a];
+    uint8_t *zt = A.codes + (size_t)tile * D * D;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        float rc[8];
+        float amax = 0.0f;
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+            rc[a] = (float)m[a][b] * ic[a];
+            amax = fmaxf(amax, fabsf(rc[a]));
+        }
+        amax = row16_max(amax);
+        const float dl = amax > 0.0f ? amax / QMAX : 0.0f;
+        const float inv = amax > 0.0f ? QMAX / amax : 0.0f;
+        uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+            uint32_t code;
+            if (CODE) {
+                const float t = fminf(fmaxf(rc[a] * inv, -448.0f), 448.0f);
+                code = f_to_e4m3(t);
+            } else {
+                const float t = fminf(fmaxf(rintf(rc[a] * inv), -127.0f), 127.0f);
+                code = (uint32_t)(uint8_t)(int8_t)t;
+            }
+            if (a < 4) w0 |= code << (8 * a);
+            else w1 |= code << (8 * (a - 4));
+        }
+        *(uint2 *)(zt + (size_t)(8 * vb + b) * D + 8 * kb) = make_uint2(w0, w1);
+        if (kb == 0) A.scale[tvec + 8 * vb + b] = dl;
+    }
+    if (tid == 0) A.rec_len[tile] = 0;
+}
+
+template <int GATE, int CODE, int MODE>
+hipError_t launch3(const TileArgs &a, int tiles, hipStream_t st) {
+    hipLaunchKernelGGL((tile_kernel<GATE, CODE, MODE>), dim3(tiles), dim3(NT), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int GATE, int CODE>
+hipError_t launch2(const TileArgs &a, int tiles, int mode, hipStream_t st) {
+    switch (mode) {
+        case TILE_QUANTIZE: return launch3<GATE, CODE, TILE_QUANTIZE>(a, tiles, st);
+        case TILE_COMMIT: return launch3<GATE, CODE, TILE_COMMIT>(a, tiles, st);
+        default: return launch3<GATE, CODE, TILE_DEQUANT>(a, tiles, st);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_tile(const lq_dims &d, const StatePtrs &s, int mode, const float *S_in,
+                       float *S_out, const int32_t *mask, hipStream_t st) {
+    TileArgs a;
+    a.codes = (uint8_t *)s.codes;
+    a.scale = s.scale;
+    a.smooth = s.smooth;
+    a.comp_k = s.comp_k;
+    a.comp_u = s.comp_u;
+    a.rec_k = s.rec_k;
+    a.rec_u = s.rec_u;
+    a.rec_a = s.rec_a;
+    a.rec_len = s.rec_len;
+    a.err = s.err;
+    a.S_in = S_in;
+    a.S_out = S_out;
+    a.mask = mask;
+    a.heads_v = d.heads_v;
+    a.window = d.window;
+    a.n_comp = d.n_comp;
+    a.power_iters = d.power_iters;
+    a.smooth_on = d.smooth;
+    const int tiles = d.batch * d.heads_v;
+    const bool kda = d.gate == LQ_GATE_DIAG, e4 = d.code == LQ_CODE_E4M3;
+    if (kda) return e4 ? launch2<1, 1>(a, tiles, mode, st) : launch2<1, 0>(a, tiles, mode, st);
+    return e4 ? launch2<0, 1>(a, tiles, mode, st) : launch2<0, 0>(a, tiles, mode, st);
+}
+
+}  // namespace lq

@@ -1,0 +1,352 @@
+"""GPU parity of every kernel behind the C ABI against the CPU oracle.
+
+Bars: outputs and dequantized states within relative L2 1e-3 per tile, INT8 /
+E4M3 codes equal in >= 99.9 % of entries and at most one grid step apart
+elsewhere, FP16 records bit-equal in >= 99.9 % of entries.  Code-level
+parity is checked window by window (the GPU starts each window from the
+oracle's representation): a free-running fp32 trajectory and an fp64 one drift
+apart at the level of the quantization noise itself, because any rounding
+decision that flips propagates, so free-running runs are checked by properties.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_38166_amd import binding as B
+from paper_2609_38166_amd import synth
+from tests import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+
+W_ = synth.WORKLOADS
+SMALL = {
+    "gdn_tiny": W_["gdn_tiny"],
+    "kda_small": W_["kda_kimi"].with_(name="kda_small", batch=2, heads_v=4, heads_k=4, steps=128,
+                                      prefill=256),
+    "gqa_int8_small": W_["gdn_qwen3next"].with_(name="gqa_int8_small", batch=2, heads_v=4,
+                                                heads_k=2, steps=128, prefill=256),
+    "gqa_e4m3_small": W_["gdn_qwen3next"].with_(name="gqa_e4m3_small", batch=2, heads_v=4,
+                                                heads_k=2, steps=128, prefill=256,
+                                                code=synth.CODE_E4M3),
+    "stress_small": W_["gdn_stress"].with_(name="stress_small", batch=4, heads_v=32, heads_k=32,
+                                           steps=64, prefill=128),
+    "kda_w16_r4": W_["kda_kimi"].with_(name="kda_w16_r4", batch=2, heads_v=4, heads_k=4, steps=64,
+                                       window=16, n_comp=4, prefill=128),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _tokens_random(wl, T, seed):
+    st = synth.Streams(wl.with_(seed=seed), synth.PHASE_DECODE)
+    tok = st.draw(T)
+    st.close()
+    return st, tok
+
+
+@pytest.mark.parametrize("gate", [synth.GATE_SCALAR, synth.GATE_DIAG])
+@pytest.mark.parametrize("dtype", [B.LQ_STATE_F32, B.LQ_STATE_BF16])
+def test_baseline_step_parity(gate, dtype):
+    wl = W_["gdn_tiny"].with_(batch=2, heads_v=4, heads_k=2, gate=gate)
+    H.log(f"baseline gate={gate} dtype={dtype}")
+    rng = np.random.default_rng(5)
+    S0 = rng.standard_normal((wl.tiles, wl.dk, wl.dv)).astype(np.float32).astype(np.float64)
+    if dtype == B.LQ_STATE_BF16:
+        S0 = O.f32_to_bf16_bits(S0.astype(np.float32)).astype(np.uint32) << 16
+        S0 = S0.view(np.float32).astype(np.float64)
+    streams, tok = _tokens_random(wl, 24, 77)
+    o_ref, S_ref = O.run_baseline(H.ocfg(wl), S0, synth.tile_major(wl, streams, tok),
+                                  mode=O.STATE_F32 if dtype == B.LQ_STATE_F32 else O.STATE_BF16)
+    dims = H.gdims(wl)
+    S_t = np.ascontiguousarray(S0.transpose(0, 2, 1)).astype(np.float32)
+    if dtype == B.LQ_STATE_BF16:
+        S_g = H.dev(S_t).to(torch.bfloat16)
+    else:
+        S_g = H.dev(S_t)
+    dt = H.DeviceTokens(wl, tok)
+    o = torch.empty((wl.tiles, wl.dv), dtype=torch.float32, device="cuda")
+    outs = []
+    for t in range(24):
+        B.leapquant_baseline_step(dims, S_g, dtype, *dt.step(t), o)
+        outs.append(o.cpu().numpy())
+    og = np.stack(outs, axis=1)
+    Sg = S_g.float().cpu().numpy().transpose(0, 2, 1)
+    tol = 1e-5 if dtype == B.LQ_STATE_F32 else 2e-3
+    assert H.rel_rows(og, o_ref) < tol
+    assert H.rel_rows(Sg.reshape(wl.tiles, -1), S_ref.reshape(wl.tiles, -1)) < tol
+    if dtype == B.LQ_STATE_BF16:
+        # the stored state is bf16 with its values mostly equal to the oracle's
+        ref_bits = O.f32_to_bf16_bits(S_ref.astype(np.float32))
+        got_bits = S_g.view(torch.int16).cpu().numpy().view(np.uint16).transpose(0, 2, 1)
+        assert np.mean(ref_bits == got_bits) > 0.99
+
+
+def test_prefill_parity_fp32():
+    """512-token fp32 prefill of the tiny GDN workload (the initial-state recipe)."""
+    wl = W_["gdn_tiny"]
+    st = synth.Streams(wl, synth.PHASE_PREFILL)
+    tok = st.draw(wl.prefill)
+    _, S_ref = O.run_baseline(H.ocfg(wl), np.zeros((wl.tiles, 128, 128)),
+                              synth.tile_major(wl, st, tok), mode=O.STATE_F32, want_o=False)
+    dims = H.gdims(wl)
+    S_g = torch.zeros((wl.tiles, 128, 128), dtype=torch.float32, device="cuda")
+    dt = H.DeviceTokens(wl, tok)
+    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+    for t in range(wl.prefill):
+        B.leapquant_baseline_step(dims, S_g, B.LQ_STATE_F32, *dt.step(t), o)
+    Sg = S_g.cpu().numpy().transpose(0, 2, 1)
+    assert H.rel_rows(Sg.reshape(wl.tiles, -1), S_ref.reshape(wl.tiles, -1)) < 1e-5
+
+
+def _states_with_edges(n, seed):
+    rng = np.random.default_rng(seed)
+    S = []
+    for i in range(n):
+        s = sum(np.outer(rng.standard_normal(128), rng.standard_normal(128)) * 0.7 ** j for j in range(6))
+        s = s + 0.3 * rng.standard_normal((128, 128))
+        s[rng.choice(128, 2, replace=False), :] *= 20
+        s[:, rng.choice(128, 2, replace=False)] *= 20
+        S.append(s)
+    S = np.stack(S)
+    S[1] = 0.0                                   # all-zero tile
+    S[2][:, [5, 99]] = 0.0                       # zero value columns
+    S[3] = np.outer(rng.standard_normal(128), rng.standard_normal(128))   # rank one
+    return S.astype(np.float32).astype(np.float64)   # both sides get the same fp32 values
+
+
+@pytest.mark.parametrize("code", [synth.CODE_INT8, synth.CODE_E4M3])
+@pytest.mark.parametrize("r", [0, 4, 8])
+@pytest.mark.parametrize("smooth", [0, 1])
+def test_quantize_state_parity(code, r, smooth):
+    H.log(f"quantize code={code} r={r} smooth={smooth}")
+    wl = W_["gdn_tiny"].with_(batch=4, heads_v=8, heads_k=8, n_comp=r, code=code)
+    S = _states_with_edges(wl.tiles, 100 + r)
+    cfg = H.ocfg(wl, smooth=smooth)
+    exp = {"Z": [], "delta": [], "c": [], "Kt": [], "Ut": []}
+    for i in range(wl.tiles):
+        rep = O.quantize(cfg, S[i])
+        for k_ in exp:
+            exp[k_].append(getattr(rep, k_))
+    exp = {k_: np.stack(v_) for k_, v_ in exp.items()}
+    dims = H.gdims(wl, smooth=smooth)
+    st = B.State.empty(dims)
+    st.rec_len.fill_(5)
+    B.leapquant_quantize_state(dims, H.dev(S.transpose(0, 2, 1).astype(np.float32)), st)
+    got = H.download_rep(st)
+    assert np.all(got["rec_len"] == 0)
+    cr = H.compare_rep(cfg, got, exp, code)
+    H.log(cr)
+    assert cr["code_eq"] >= 0.999 and cr["code_maxdiff"] <= 1, cr
+    assert cr["deq_rel"] <= 1e-3 and cr["delta_rel"] <= 1e-5 and cr["c_rel"] <= 1e-5, cr
+    if r:
+        assert cr["comp_rel"] <= 1e-3, cr
+    assert not got["Z"][1].any() and not got["delta"][1].any()
+    assert got["delta"][2][5] == 0 and got["delta"][2][99] == 0
+
+
+@pytest.mark.parametrize("name", ["gdn_tiny", "kda_small", "gqa_e4m3_small"])
+def test_dequantize_state_parity(name):
+    """Base + open-window records, materialised on the GPU from the oracle's
+    representation and records, equals the oracle's dense window state."""
+    wl = SMALL[name]
+    H.log(f"dequantize {name}")
+    cfg = H.ocfg(wl)
+    S0 = H.oracle_prefill_state(wl)
+    streams, tok = H.decode_tokens(wl, n=wl.window + wl.window // 2 + 1)
+    ref = O.run_dense(cfg, S0, synth.tile_major(wl, streams, tok), snapshots=True)
+    n = int(ref["rec_len"][0])
+    assert n > 0
+    dims = H.gdims(wl)
+    st = B.State.empty(dims)
+    H.upload_rep(st, np.arange(wl.tiles), ref["Z"][:, 1], ref["delta"][:, 1], ref["c"][:, 1],
+                 ref["Kt"][:, 1], ref["Ut"][:, 1])
+    W, g = wl.window, wl.g
+    st.rec_a.view(wl.tiles, W, g)[:] = H.dev(ref["rec_a"].astype(np.float16))
+    st.rec_k.view(wl.tiles, W, wl.dk)[:] = H.dev(ref["rec_k"].astype(np.float16))
+    st.rec_u.view(wl.tiles, W, wl.dv)[:] = H.dev(ref["rec_u"].astype(np.float16))
+    st.rec_len.fill_(n)
+    S_out = torch.empty((wl.tiles, 128, 128), dtype=torch.float32, device="cuda")
+    B.leapquant_dequantize_state(dims, st, S_out)
+    Sg = S_out.cpu().numpy().transpose(0, 2, 1)
+    assert H.rel_rows(Sg.reshape(wl.tiles, -1), ref["S_final"].reshape(wl.tiles, -1)) < 1e-5
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_window_synchronised_parity(name):
+    wl = SMALL[name]
+    H.log(f"window-sync {name}")
+    H.window_sync_parity(wl)
+
+
+def test_free_running_tiny():
+    """The whole GDN tiny trajectory on the GPU alone (its own fp32 prefill, its own
+    quantization, 256 decode steps, 16 commits).  Properties: the GPU's error
+    against the unquantized fp32 trajectory matches the oracle's, and both
+    quantized trajectories agree to well within that error."""
+    wl = W_["gdn_tiny"]
+    H.log("free-running gdn_tiny")
+    cfg = H.ocfg(wl)
+    S0 = H.oracle_prefill_state(wl)
+    streams, tok = H.decode_tokens(wl)
+    otok = synth.tile_major(wl, streams, tok)
+    ref = O.run_dense(cfg, S0, otok, snapshots=False)
+    o_fp, _ = O.run_baseline(cfg, S0, otok, mode=O.STATE_F32)
+    # GPU: prefill with its own fp32 baseline kernel, outliers, quantize, decode
+    dims = H.gdims(wl)
+    pst = synth.Streams(wl, synth.PHASE_PREFILL)
+    ptok = pst.draw(wl.prefill)
+    pdt = H.DeviceTokens(wl, ptok)
+    S_g = torch.zeros((wl.tiles, 128, 128), dtype=torch.float32, device="cuda")
+    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+    for t in range(wl.prefill):
+        B.leapquant_baseline_step(dims, S_g, B.LQ_STATE_F32, *pdt.step(t), o)
+    F = synth.outlier_factor(synth.outliers(wl))
+    S_g *= H.dev(np.ascontiguousarray(F.transpose(0, 2, 1)))
+    st = B.State.empty(dims)
+    B.leapquant_quantize_state(dims, S_g, st)
+    dt = H.DeviceTokens(wl, tok)
+    outs = []
+    for t in range(wl.steps):
+        B.leapquant_decode_step(dims, st, *dt.step(t), o)
+        outs.append(o.cpu().numpy())
+        if (t + 1) % wl.window == 0:
+            B.leapquant_window_commit(dims, st)
+    og = np.stack(outs, axis=1)
+    assert np.all(np.isfinite(og))
+    assert B.leapquant_check_error(st) == 0
+    e_gpu = H.rel(og, o_fp)
+    e_orc = H.rel(ref["o"], o_fp)
+    d = H.rel(og, ref["o"])
+    H.log(f"free-running: gpu-vs-fp32 {e_gpu:.3e} oracle-vs-fp32 {e_orc:.3e} gpu-vs-oracle {d:.3e}")
+    assert 0.5 < e_gpu / e_orc < 2.0
+    assert d < max(2.0 * e_orc, 1e-3)
+
+
+def test_partial_windows_mask_and_reset():
+    """Ragged schedule: tokens 0..20 then a commit of request 0 only, more tokens,
+    a commit of everything (partial windows), and a commit on empty windows."""
+    wl = SMALL["kda_small"].with_(steps=40)
+    cfg = H.ocfg(wl)
+    S0 = H.oracle_prefill_state(wl)
+    streams, tok = H.decode_tokens(wl)
+    otok = synth.tile_major(wl, streams, tok)
+    dims = H.gdims(wl)
+    st = B.State.empty(dims)
+    rep0 = O.run_dense(cfg, S0, {k_: v_[:, :0] for k_, v_ in otok.items()}, snapshots=True)
+    H.upload_rep(st, np.arange(wl.tiles), rep0["Z"][:, 0], rep0["delta"][:, 0], rep0["c"][:, 0],
+                 rep0["Kt"][:, 0], rep0["Ut"][:, 0])
+    dt = H.DeviceTokens(wl, tok)
+    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+    for t in range(21):
+        B.leapquant_decode_step(dims, st, *dt.step(t), o)
+    mask = torch.tensor([1, 0], dtype=torch.int32, device="cuda")
+    before = H.download_rep(st)
+    B.leapquant_window_commit(dims, st, mask)
+    after = H.download_rep(st)
+    h = wl.heads_v
+    assert np.all(after["rec_len"][:h] == 0) and np.all(after["rec_len"][h:] == 21)
+    for k_ in ("Z", "delta", "c", "Kt", "Ut"):
+        assert np.array_equal(after[k_][h:], before[k_][h:])       # unselected: untouched
+    # request 0 committed a partial window of 21 tokens from its own records:
+    # against the oracle's quantization of its dense state after 21 tokens
+    sub = {k_: v_[:h, :21] for k_, v_ in otok.items()}
+    ref = O.run_dense(cfg, S0[:h], sub, snapshots=False, history=True)
+    exp = {"Z": [], "delta": [], "c": [], "Kt": [], "Ut": []}
+    for i in range(h):
+        rp = O.quantize(cfg, ref["S_final"][i])
+        for k_ in exp:
+            exp[k_].append(getattr(rp, k_))
+    exp = {k_: np.stack(v_) for k_, v_ in exp.items()}
+    got = {k_: after[k_][:h] for k_ in ("Z", "delta", "c", "Kt", "Ut")}
+    cr = H.compare_rep(cfg, got, exp, wl.code)
+    H.log("partial chained", cr)
+    assert cr["code_eq"] >= 0.99 and cr["deq_rel"] <= 1e-2, cr
+    # the same partial commit from the oracle's records is exact
+    st2 = B.State.empty(dims)
+    H.upload_rep(st2, np.arange(wl.tiles), rep0["Z"][:, 0], rep0["delta"][:, 0], rep0["c"][:, 0],
+                 rep0["Kt"][:, 0], rep0["Ut"][:, 0])
+    full = O.run_dense(cfg, S0, {k_: v_[:, :21] for k_, v_ in otok.items()}, snapshots=False,
+                       history=True)
+    H.upload_records(st2, full["hist_a"], full["hist_k"], full["hist_u"])
+    B.leapquant_window_commit(dims, st2, mask)
+    got2 = H.download_rep(st2)
+    got2 = {k_: got2[k_][:h] for k_ in ("Z", "delta", "c", "Kt", "Ut")}
+    cr2 = H.compare_rep(cfg, got2, exp, wl.code)
+    assert cr2["code_eq"] >= 0.999 and cr2["code_maxdiff"] <= 1 and cr2["deq_rel"] <= 1e-3, cr2
+    assert cr2["delta_rel"] <= 1e-5 and cr2["c_rel"] <= 1e-5, cr2
+    # empty windows: commit is a no-op
+    snap = H.download_rep(st)
+    B.leapquant_window_commit(dims, st, torch.tensor([1, 0], dtype=torch.int32, device="cuda"))
+    again = H.download_rep(st)
+    for k_ in ("Z", "delta", "c", "Kt", "Ut", "rec_len"):
+        assert np.array_equal(again[k_], snap[k_])
+    B.leapquant_window_commit(dims, st)     # all: request 1 commits its 21 records
+    assert np.all(H.download_rep(st)["rec_len"] == 0)
+    assert B.leapquant_check_error(st) == 0
+
+
+def test_full_window_raises_device_error_and_leaves_state():
+    wl = SMALL["gdn_tiny"].with_(window=2, steps=3)
+    dims = H.gdims(wl)
+    cfg = H.ocfg(wl)
+    S0 = H.oracle_prefill_state(wl.with_(prefill=32))
+    st = B.State.empty(dims)
+    rep = O.run_dense(cfg, S0, {k_: v_[:, :0] for k_, v_ in synth.tile_major(
+        wl, *H.decode_tokens(wl)).items()}, snapshots=True)
+    H.upload_rep(st, np.arange(wl.tiles), rep["Z"][:, 0], rep["delta"][:, 0], rep["c"][:, 0],
+                 rep["Kt"][:, 0], rep["Ut"][:, 0])
+    _, tok = H.decode_tokens(wl)
+    dt = H.DeviceTokens(wl, tok)
+    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+    B.leapquant_decode_step(dims, st, *dt.step(0), o)
+    B.leapquant_decode_step(dims, st, *dt.step(1), o)
+    assert B.leapquant_check_error(st) == 0
+    before = {f: getattr(st, f).clone() for f in B.FIELDS if f != "err"}
+    B.leapquant_decode_step(dims, st, *dt.step(2), o)
+    assert torch.isnan(o).all()
+    assert B.leapquant_check_error(st) == B.LQ_DEVERR_WINDOW_FULL
+    assert B.leapquant_check_error(st) == 0          # cleared
+    for f, t in before.items():
+        assert torch.equal(getattr(st, f), t), f
+
+
+def test_corrupt_window_length_is_rejected_on_device():
+    wl = SMALL["gdn_tiny"].with_(window=4)
+    dims = H.gdims(wl)
+    st = B.State.empty(dims)
+    st.rec_len.fill_(7)
+    S_out = torch.zeros((wl.tiles, 128, 128), dtype=torch.float32, device="cuda")
+    B.leapquant_dequantize_state(dims, st, S_out)
+    B.leapquant_window_commit(dims, st)
+    assert B.leapquant_check_error(st) == B.LQ_DEVERR_BAD_REC_LEN
+    assert not S_out.any() and torch.all(st.rec_len == 7)
+
+
+def test_decode_is_deterministic():
+    wl = SMALL["kda_small"].with_(steps=20)
+    dims = H.gdims(wl)
+    S0 = H.oracle_prefill_state(wl)
+    _, tok = H.decode_tokens(wl)
+    dt = H.DeviceTokens(wl, tok)
+    res = []
+    for _ in range(2):
+        st = B.State.empty(dims)
+        B.leapquant_quantize_state(dims, H.dev(S0.transpose(0, 2, 1).astype(np.float32)), st)
+        o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+        outs = []
+        for t in range(20):
+            B.leapquant_decode_step(dims, st, *dt.step(t), o)
+            outs.append(o.clone())
+            if t == 9:
+                B.leapquant_window_commit(dims, st)
+        res.append((torch.stack(outs), st.codes.clone(), st.comp_u.clone(), st.rec_u.clone()))
+    for a, b in zip(res[0], res[1]):
+        assert torch.equal(a, b)
