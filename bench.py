@@ -1,0 +1,379 @@
+"""Throughput of the LeapQuant 8-bit decode path on one MI355X.
+
+One benchmark step is one pass of the whole hot path over one batch: the
+window-start quantization of the prefill state (leapquant_quantize_state),
+then T decode tokens (one leapquant_decode_step launch per token over every
+(request, head) tile) with a leapquant_window_commit after every W tokens.
+The metric is token-head decode steps per second (tiles x T / time), reported
+with the effective HBM bandwidth of the algorithmic bytes, its fraction of the
+8 TB/s peak, and the speedup over the per-step bf16 and fp32 dense-state
+baselines run on the same tokens.
+
+Inputs are synthetic and seeded (paper_2609_38166_amd.synth): they are
+generated on the host, copied to HBM before the timed region, and the initial
+state is built on the GPU by an fp32 prefill recurrence plus outlier lines.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="kda_kimi")
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
+    ap.add_argument("--no-baselines", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tiles", type=int, default=1024)
+    ap.add_argument("--profile", action="store_true",
+                    help="short run for profilers: setup, warmup and the timed steps only")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------- bytes
+
+def rec_bytes(wl):
+    return 2 * (wl.dk + wl.dv) + 2 * wl.g          # FP16 key, correction, decay
+
+
+def decode_bytes(wl, i):
+    """Algorithmic bytes of one tile's decode at window position i (1-based)."""
+    inputs = 4 * (2 * wl.dk) * wl.heads_k / wl.heads_v + 4 * wl.dv + 4 * wl.g + 4
+    return (wl.dk * wl.dv + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+            + (i - 1) * rec_bytes(wl) + rec_bytes(wl) + inputs + 4 * wl.dv + 8)
+
+
+def rep_bytes(wl):
+    return wl.dk * wl.dv + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+
+
+def commit_bytes(wl, p):
+    return rep_bytes(wl) + p * rec_bytes(wl) + rep_bytes(wl) + 8
+
+
+def quantize_bytes(wl):
+    return 4 * wl.dk * wl.dv + rep_bytes(wl) + 4
+
+
+def baseline_bytes(wl, width):
+    inputs = 4 * (2 * wl.dk) * wl.heads_k / wl.heads_v + 4 * wl.dv + 4 * wl.g + 4
+    return 2 * width * wl.dk * wl.dv + inputs + 4 * wl.dv
+
+
+# ----------------------------------------------------------------------------- setup
+
+def device_tokens(wl, phase, T, chunk=64):
+    """Step-major device tensors of T tokens, generated in chunks on the host."""
+    import torch
+    from paper_2609_38166_amd import synth
+    B, Hv, Hk = wl.batch, wl.heads_v, wl.heads_k
+    q = torch.empty((T, B, Hk, wl.dk), dtype=torch.float32, device="cuda")
+    k = torch.empty_like(q)
+    v = torch.empty((T, B, Hv, wl.dv), dtype=torch.float32, device="cuda")
+    a = torch.empty((T, B, Hv, wl.dk) if wl.gate == synth.GATE_DIAG else (T, B, Hv),
+                    dtype=torch.float32, device="cuda")
+    b = torch.empty((T, B, Hv), dtype=torch.float32, device="cuda")
+    st = synth.Streams(wl, phase)
+    for t0 in range(0, T, chunk):
+        n = min(chunk, T - t0)
+        sm = synth.step_major_full(wl, st.draw(n))
+        for dst, key in ((q, "q"), (k, "k"), (v, "v"), (a, "alpha"), (b, "beta")):
+            dst[t0:t0 + n].copy_(torch.from_numpy(sm[key]))
+    st.close()
+    return q, k, v, a, b
+
+
+def prefill_state(wl, dims):
+    """Initial states S^T [B][Hv][dv][dk]: fp32 prefill on the GPU, then outliers."""
+    import torch
+    from paper_2609_38166_amd import binding as B_, synth
+    S = torch.zeros((wl.batch, wl.heads_v, wl.dv, wl.dk), dtype=torch.float32, device="cuda")
+    o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+    st = synth.Streams(wl, synth.PHASE_PREFILL)
+    chunk = 64
+    for t0 in range(0, wl.prefill, chunk):
+        n = min(chunk, wl.prefill - t0)
+        sm = synth.step_major_full(wl, st.draw(n))
+        dev = {kk: torch.from_numpy(vv).cuda() for kk, vv in sm.items()}
+        for t in range(n):
+            B_.leapquant_baseline_step(dims, S, B_.LQ_STATE_F32, dev["q"][t], dev["k"][t],
+                                       dev["v"][t], dev["alpha"][t], dev["beta"][t], o)
+    st.close()
+    out = synth.outliers(wl)
+    rf = torch.from_numpy(out["row_f"]).cuda().view(wl.batch, wl.heads_v, 1, wl.dk)
+    cf = torch.from_numpy(out["col_f"]).cuda().view(wl.batch, wl.heads_v, wl.dv, 1)
+    S *= torch.maximum(rf, cf)
+    torch.cuda.synchronize()
+    return S
+
+
+# ----------------------------------------------------------------------------- timing
+
+class Runner:
+    def __init__(self, wl, dims, S0, toks, use_graph):
+        import torch
+        from paper_2609_38166_amd import binding as B_
+        self.wl, self.dims, self.S0, self.toks = wl, dims, S0, toks
+        self.B_ = B_
+        self.st = B_.State.empty(dims)
+        self.o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+        self.graph = None
+        if use_graph:
+            self._capture()
+
+    def _calls(self):
+        """Prepared launches of one step on the current stream."""
+        B_, wl, d, st = self.B_, self.wl, self.dims, self.st
+        q, k, v, a, b = self.toks
+        calls = []
+        s = st.struct()
+        self._keep = [s]
+        L = B_.lib()
+        import ctypes as C
+        stream = B_._stream(None)
+        calls.append(B_.Prepared(L.leapquant_quantize_state, C.byref(d), self.S0.data_ptr(),
+                                 C.byref(s), stream))
+        for t in range(wl.steps):
+            calls.append(B_.Prepared(L.leapquant_decode_step, C.byref(d), C.byref(s), q[t].data_ptr(),
+                                     k[t].data_ptr(), v[t].data_ptr(), a[t].data_ptr(),
+                                     b[t].data_ptr(), self.o.data_ptr(), stream))
+            if (t + 1) % wl.window == 0:
+                calls.append(B_.Prepared(L.leapquant_window_commit, C.byref(d), C.byref(s), None,
+                                         stream))
+        return calls
+
+    def _capture(self):
+        import torch
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for c in self._calls():     # one eager pass on the capture stream first
+                c()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            for c in self._calls():
+                c()
+        torch.cuda.synchronize()
+
+    def step(self):
+        if self.graph is not None:
+            self.graph.replay()
+        else:
+            for c in self._calls_cache():
+                c()
+
+    def _calls_cache(self):
+        if not hasattr(self, "_cc"):
+            self._cc = self._calls()
+        return self._cc
+
+
+def time_steps(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) / 1e3, wall
+
+
+def per_launch_times(wl, dims, S0, toks):
+    """HIP-event durations of every decode launch of one window (all positions),
+    of the commit that ends it and of the window-start quantization, measured
+    on the stream the kernels run on."""
+    import torch
+    from paper_2609_38166_amd import binding as B_
+    st = B_.State.empty(dims)
+    o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+    q, k, v, a, b = toks
+    W = wl.window
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(W + 2)]
+    res = {"decode": [], "commit": [], "quantize": []}
+    for rep in range(3):
+        ev[0][0].record()
+        B_.leapquant_quantize_state(dims, S0, st)
+        ev[0][1].record()
+        for i in range(W):
+            ev[i + 1][0].record()
+            B_.leapquant_decode_step(dims, st, q[i], k[i], v[i], a[i], b[i], o)
+            ev[i + 1][1].record()
+        ev[W + 1][0].record()
+        B_.leapquant_window_commit(dims, st)
+        ev[W + 1][1].record()
+        torch.cuda.synchronize()
+        if rep == 0:
+            continue                      # first pass warms caches and clocks
+        res["quantize"].append(ev[0][0].elapsed_time(ev[0][1]))
+        res["decode"].append([ev[i + 1][0].elapsed_time(ev[i + 1][1]) for i in range(W)])
+        res["commit"].append(ev[W + 1][0].elapsed_time(ev[W + 1][1]))
+    dec = np.mean(np.array(res["decode"]), axis=0)   # ms per position
+    return {"decode_ms_by_pos": dec, "decode_ms": float(dec.mean()),
+            "commit_ms": float(np.mean(res["commit"])), "quantize_ms": float(np.mean(res["quantize"]))}
+
+
+def cpu_baseline(wl, n_tiles):
+    """The CPU oracle (fp64, OpenMP over tiles) on a bounded sample of the same
+    workload: window-start quantization, all T tokens and the commits."""
+    from oracle import oracle as O
+    from paper_2609_38166_amd import synth
+    tiles = np.linspace(0, wl.tiles - 1, n_tiles).astype(int)
+    cfg = O.make_cfg(dk=wl.dk, dv=wl.dv, window=wl.window, n_comp=wl.n_comp,
+                     power_iters=wl.power_iters, gate=wl.gate, code=wl.code)
+    pst = synth.Streams(wl, synth.PHASE_PREFILL, tiles)
+    ptok = synth.tile_major(wl, pst, pst.draw(wl.prefill))
+    _, Sp = O.run_baseline(cfg, np.zeros((n_tiles, wl.dk, wl.dv)), ptok, mode=O.STATE_F32,
+                           want_o=False)
+    F = synth.outlier_factor(synth.outliers(wl, tiles))
+    S0 = (Sp.astype(np.float32) * F).astype(np.float64)
+    dst = synth.Streams(wl, synth.PHASE_DECODE, tiles)
+    tok = synth.tile_major(wl, dst, dst.draw(wl.steps))
+    threads = O.default_threads()
+    t0 = time.perf_counter()
+    O.run_dense(cfg, S0, tok, snapshots=False, threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": round(n_tiles * wl.steps / dt, 1), "unit": "token-head steps/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"{n_tiles} of {wl.tiles} tiles (evenly spaced), all {wl.steps} tokens, "
+                      f"quantize + decode + commits in fp64, {dt:.2f} s"}
+
+
+# ----------------------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the decode path has no "
+              "cross-GPU step -- tiles shard by request and head", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_38166_amd import binding as B_, synth
+    B_.lib()
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=wl.window, n_comp=wl.n_comp,
+                        power_iters=wl.power_iters, gate=wl.gate, code=wl.code)
+    t0 = time.time()
+    log(f"[bench] {wl.name}: tiles={wl.tiles} T={wl.steps} W={wl.window} r={wl.n_comp}")
+    toks = device_tokens(wl, synth.PHASE_DECODE, wl.steps)
+    log(f"[bench] decode inputs on device ({time.time() - t0:.1f}s)")
+    S0 = prefill_state(wl, dims)
+    log(f"[bench] prefill done ({time.time() - t0:.1f}s)")
+
+    runner = Runner(wl, dims, S0, toks, use_graph=not args.no_graph)
+    log("[bench] runner ready")
+    secs, wall = time_steps(runner.step, args.steps, args.warmup)
+    ms_step = secs / args.steps * 1e3
+    tile_steps = wl.tiles * wl.steps
+    value = tile_steps * args.steps / secs
+    log(f"[bench] leapquant {ms_step:.3f} ms/step, {value:.4g} token-head steps/s")
+    if args.profile:
+        print(json.dumps({"profile_ms_per_step": ms_step}), flush=True)
+        return
+
+    kt = per_launch_times(wl, dims, S0, toks)
+    W = wl.window
+    dec_bytes = [decode_bytes(wl, i) * wl.tiles for i in range(1, W + 1)]
+    dec_avg_bytes = float(np.mean(dec_bytes))
+    achieved = dec_avg_bytes / (kt["decode_ms"] * 1e-3) / 1e9
+    step_bytes = (sum(dec_bytes) * (wl.steps // W) + commit_bytes(wl, W) * wl.tiles * (wl.steps // W)
+                  + quantize_bytes(wl) * wl.tiles)
+    eff = step_bytes / (ms_step * 1e-3) / 1e9
+    log(f"[bench] decode {kt['decode_ms'] * 1e3:.1f} us/launch ({achieved:.0f} GB/s), "
+        f"commit {kt['commit_ms'] * 1e3:.1f} us, quantize {kt['quantize_ms'] * 1e3:.1f} us")
+
+    out = {
+        "metric": "token-head decode steps/s + effective HBM GB/s (% of peak), speedup vs bf16 state",
+        "value": round(value, 1),
+        "unit": "token-head steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: KDA (per-channel gate) batch {wl.batch}, {wl.heads_v} heads, "
+                               f"d_k=d_v={wl.dk}, {wl.steps} decode tokens, W={wl.window}, "
+                               f"r={wl.n_comp}, int8 state" if wl.gate == synth.GATE_DIAG else wl.name,
+                   "tiles": wl.tiles, "tokens": wl.steps, "window": wl.window, "n_comp": wl.n_comp,
+                   "graph": not args.no_graph},
+        "effective_gbps": round(eff, 1),
+        "frac_of_hbm_peak": round(eff / PEAK_HBM_GBS, 4),
+        "roofline": {"kernel": "decode_step", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": None,
+                     "bytes_per_launch": round(dec_avg_bytes), "avg_launch_us": round(kt["decode_ms"] * 1e3, 2)},
+        "kernels_us": {"decode_avg": round(kt["decode_ms"] * 1e3, 2),
+                       "decode_first_pos": round(float(kt["decode_ms_by_pos"][0]) * 1e3, 2),
+                       "decode_last_pos": round(float(kt["decode_ms_by_pos"][-1]) * 1e3, 2),
+                       "commit": round(kt["commit_ms"] * 1e3, 2),
+                       "quantize": round(kt["quantize_ms"] * 1e3, 2)},
+    }
+
+    if not args.no_baselines:
+        q, k, v, a, b = toks
+        res = {}
+        for name, dtype, width, tdt in (("bf16", B_.LQ_STATE_BF16, 2, torch.bfloat16),
+                                        ("fp32", B_.LQ_STATE_F32, 4, torch.float32)):
+            S = S0.to(tdt).contiguous()
+            o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+
+            def run(S=S, o=o, dtype=dtype):
+                for t in range(wl.steps):
+                    B_.leapquant_baseline_step(dims, S, dtype, q[t], k[t], v[t], a[t], b[t], o)
+            g = None
+            if not args.no_graph:
+                run()
+                torch.cuda.synchronize()
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    run()
+            fn = g.replay if g is not None else run
+            bs, _ = time_steps(fn, args.steps, args.warmup)
+            rate = tile_steps * args.steps / bs
+            gbs = baseline_bytes(wl, width) * tile_steps * args.steps / bs / 1e9
+            res[name] = {"value": round(rate, 1), "ms_per_step": round(bs / args.steps * 1e3, 4),
+                         "effective_gbps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
+            log(f"[bench] {name} baseline {res[name]}")
+            del S
+        out["baselines"] = res
+        out["speedup_vs_bf16"] = round(value / res["bf16"]["value"], 3)
+        out["speedup_vs_fp32"] = round(value / res["fp32"]["value"], 3)
+        out["byte_ratio_bound_vs_bf16"] = round(
+            baseline_bytes(wl, 2) * wl.steps / (step_bytes / wl.tiles), 3)
+
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_sample_tiles, wl.tiles))
+        log(f"[bench] cpu baseline {out['cpu_baseline']}")
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

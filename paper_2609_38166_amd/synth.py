@@ -6,7 +6,7 @@ holds none of the method's arithmetic, so both the HIP path (tests, benchmark)
 and the CPU oracle (tests) can be fed from it.
 
 Distributions (stand-ins for the hidden states of the paper's GDN / KDA models,
-whose weights and datasets are not available):
+whose weights and datasets are not available), all computed in float32:
   q, k  ~ N(0, I_d), then L2-normalised (the models normalise q and k);
   v     ~ N(0, I_d);
   beta  = sigmoid(N(0, 1));
@@ -101,12 +101,12 @@ def khead_of(wl: Workload, hv: int) -> int:
 class Streams:
     """Token streams of one phase for a set of value-head tiles.
 
-    ``draw(n)`` returns the next n tokens of every stream:
-      q, k      float32 [n_ktiles][n][dk]  (one row per distinct (b, key head))
-      v         float32 [n_vtiles][n][dv]
-      alpha     float32 [n_vtiles][n][g]
-      beta      float32 [n_vtiles][n]
-    ``ktile_of_vtile[i]`` maps value tile i to its key tile row.
+    ``draw(n)`` returns the next n tokens of every stream, step-major:
+      q, k      float32 [n][n_ktiles][dk]  (one row per distinct (b, key head))
+      v         float32 [n][n_vtiles][dv]
+      alpha     float32 [n][n_vtiles][g]
+      beta      float32 [n][n_vtiles]
+    ``ktile_of_vtile[i]`` maps value tile i to its key tile column.
     """
 
     def __init__(self, wl: Workload, phase: int, vtiles=None, threads=None):
@@ -126,29 +126,40 @@ class Streams:
     def draw(self, n: int) -> dict:
         wl = self.wl
         nk, nv = len(self._kg), len(self._vg)
-        qk = np.empty((nk, n, 2, wl.dk), np.float32)
-        raw = np.empty((nv, n, wl.dv + 1 + wl.g), np.float32)
+        q = np.empty((n, nk, wl.dk), np.float32)
+        k = np.empty((n, nk, wl.dk), np.float32)
+        v = np.empty((n, nv, wl.dv), np.float32)
+        beta = np.empty((n, nv), np.float32)
+        alpha = np.empty((n, nv, wl.g), np.float32)
 
-        def fill_k(i):
-            self._kg[i].standard_normal((n, 2, wl.dk), dtype=np.float32, out=qk[i])
-            x = qk[i].astype(np.float64)
-            x /= np.sqrt(np.sum(x * x, axis=-1, keepdims=True))
-            qk[i] = x.astype(np.float32)
+        def fill_k(lo, hi):
+            buf = np.empty((hi - lo, n, 2, wl.dk), np.float32)
+            for i in range(lo, hi):
+                self._kg[i].standard_normal((n, 2, wl.dk), dtype=np.float32, out=buf[i - lo])
+            buf /= np.sqrt(np.einsum("stjd,stjd->stj", buf, buf))[..., None]
+            q[:, lo:hi] = buf[:, :, 0].transpose(1, 0, 2)
+            k[:, lo:hi] = buf[:, :, 1].transpose(1, 0, 2)
 
-        def fill_v(i):
-            self._vg[i].standard_normal((n, wl.dv + 1 + wl.g), dtype=np.float32, out=raw[i])
+        def fill_v(lo, hi):
+            buf = np.empty((hi - lo, n, wl.dv + 1 + wl.g), np.float32)
+            for i in range(lo, hi):
+                self._vg[i].standard_normal(buf.shape[1:], dtype=np.float32, out=buf[i - lo])
+            v[:, lo:hi] = buf[:, :, :wl.dv].transpose(1, 0, 2)
+            zb = buf[:, :, wl.dv]
+            beta[:, lo:hi] = (np.float32(1.0) / (np.float32(1.0) + np.exp(-zb))).T
+            za = buf[:, :, wl.dv + 1:]
+            # softplus(z) = max(z, 0) + log1p(exp(-|z|))
+            sp = np.maximum(za, np.float32(0.0)) + np.log1p(np.exp(-np.abs(za)))
+            alpha[:, lo:hi] = np.exp(np.float32(-0.1) * sp).transpose(1, 0, 2)
 
-        list(self._pool.map(fill_k, range(nk)))
-        list(self._pool.map(fill_v, range(nv)))
-        zb = raw[:, :, wl.dv].astype(np.float64)
-        za = raw[:, :, wl.dv + 1:].astype(np.float64)
-        return {
-            "q": qk[:, :, 0, :].copy(),
-            "k": qk[:, :, 1, :].copy(),
-            "v": raw[:, :, :wl.dv].copy(),
-            "beta": (1.0 / (1.0 + np.exp(-zb))).astype(np.float32),
-            "alpha": np.exp(-0.1 * np.logaddexp(0.0, za)).astype(np.float32),
-        }
+        def spans(total, per=64):
+            return [(lo, min(lo + per, total)) for lo in range(0, total, per)]
+
+        futs = [self._pool.submit(fill_k, lo, hi) for lo, hi in spans(nk)]
+        futs += [self._pool.submit(fill_v, lo, hi) for lo, hi in spans(nv)]
+        for f in futs:
+            f.result()
+        return {"q": q, "k": k, "v": v, "beta": beta, "alpha": alpha}
 
     def close(self):
         self._pool.shutdown()
@@ -157,24 +168,26 @@ class Streams:
 def tile_major(wl: Workload, st: Streams, tok: dict) -> dict:
     """Per value-tile arrays [vtiles][n][...] with q, k repeated for heads sharing a key head."""
     kv = st.ktile_of_vtile
-    return {"q": tok["q"][kv], "k": tok["k"][kv], "v": tok["v"], "alpha": tok["alpha"],
-            "beta": tok["beta"]}
+    return {"q": np.ascontiguousarray(tok["q"][:, kv].transpose(1, 0, 2)),
+            "k": np.ascontiguousarray(tok["k"][:, kv].transpose(1, 0, 2)),
+            "v": np.ascontiguousarray(tok["v"].transpose(1, 0, 2)),
+            "alpha": np.ascontiguousarray(tok["alpha"].transpose(1, 0, 2)),
+            "beta": np.ascontiguousarray(tok["beta"].T)}
 
 
 def step_major_full(wl: Workload, tok: dict) -> dict:
-    """Step-major arrays for a full-batch stream set (vtiles = all tiles in order):
+    """Views for a full-batch stream set (vtiles = all tiles in order):
     q, k [n][B][Hk][dk]; v [n][B][Hv][dv]; alpha [n][B][Hv](*[dk]); beta [n][B][Hv]."""
-    n = tok["v"].shape[1]
+    n = tok["v"].shape[0]
     B, Hv, Hk = wl.batch, wl.heads_v, wl.heads_k
     out = {
-        "q": np.ascontiguousarray(tok["q"].reshape(B, Hk, n, wl.dk).transpose(2, 0, 1, 3)),
-        "k": np.ascontiguousarray(tok["k"].reshape(B, Hk, n, wl.dk).transpose(2, 0, 1, 3)),
-        "v": np.ascontiguousarray(tok["v"].reshape(B, Hv, n, wl.dv).transpose(2, 0, 1, 3)),
-        "beta": np.ascontiguousarray(tok["beta"].reshape(B, Hv, n).transpose(2, 0, 1)),
+        "q": tok["q"].reshape(n, B, Hk, wl.dk),
+        "k": tok["k"].reshape(n, B, Hk, wl.dk),
+        "v": tok["v"].reshape(n, B, Hv, wl.dv),
+        "beta": tok["beta"].reshape(n, B, Hv),
     }
-    a = tok["alpha"].reshape(B, Hv, n, wl.g)
-    out["alpha"] = np.ascontiguousarray(a.transpose(2, 0, 1, 3) if wl.gate == GATE_DIAG
-                                        else a[..., 0].transpose(2, 0, 1))
+    a = tok["alpha"]
+    out["alpha"] = a.reshape(n, B, Hv, wl.dk) if wl.gate == GATE_DIAG else a.reshape(n, B, Hv)
     return out
 
 

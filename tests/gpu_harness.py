@@ -226,7 +226,7 @@ def window_sync_parity(wl: synth.Workload, n_windows=None, check=True):
     otok = {k_: v_[:, :T] for k_, v_ in otok.items()}
     ref = O.run_dense(cfg, S0, otok, snapshots=True, history=True)
     log(f"[{wl.name}] oracle {time.time() - t0:.1f}s tiles={wl.tiles} T={T}")
-    dt = DeviceTokens(wl, {k_: v_[:, :T] for k_, v_ in tok.items()})
+    dt = DeviceTokens(wl, {k_: v_[:T] for k_, v_ in tok.items()})
     st = B.State.empty(dims)
     o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
     tiles = np.arange(wl.tiles)
