@@ -9,11 +9,14 @@
 // output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
 //
-// Memory traffic per tile: the d_v x d_k code bytes once (16-byte loads, 8
-// lanes per 128-byte row, coalesced), scales and smoothing, r token pairs, the
-// i-1 buffered records, the token's inputs, one record and the output written.
-// The decays Gamma are products of the FP16 record decays, formed on the fly
-// from the newest record backwards, so no d_k x d_v intermediate exists.
+// Every global load of the tile is issued before the first barrier: the
+// d_v x d_k code bytes (16-byte loads, 8 lanes per 128-byte row), the token
+// pairs and up to 64 records (16 slots of 16 lanes, each slot a contiguous
+// block of 4 records, 16 bytes of key, correction and decay per lane).  The
+// decays Gamma_{j+1:i} are products of the FP16 record decays: each slot forms
+// the product of its block, one scan over the 16 slots gives every block the
+// decay of all newer records, and the slot walks its block from the newest
+// record back.  No d_k x d_v intermediate exists.
 #include "lq_device.hpp"
 #include "lq_internal.hpp"
 
@@ -21,7 +24,9 @@ namespace lq {
 
 namespace {
 
-constexpr int CHUNK = 16;   // records per pass: one 16-lane group per record
+constexpr int SLOTS = 16;            // 16-lane groups per workgroup
+constexpr int PER_SLOT = 4;          // records per slot and pass
+constexpr int PASS = SLOTS * PER_SLOT;
 
 struct DecodeArgs {
     const uint8_t *codes;
@@ -46,6 +51,31 @@ struct DecodeArgs {
     int n_comp;
 };
 
+template <int GATE>
+struct RecRegs {
+    uint4 k[PER_SLOT];               // FP16 keys, 8 channels
+    uint4 u[PER_SLOT];               // FP16 corrections, 8 values
+    uint4 a[GATE ? PER_SLOT : 1];    // FP16 decays, 8 channels (diagonal gate)
+    float as[PER_SLOT];              // decay (scalar gate)
+};
+
+// Issue the loads of the records in [lo, hi) that belong to slot ts: record
+// hi-1-(PER_SLOT*ts+q) goes to register set q (newest first).
+template <int GATE>
+__device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi,
+                                             int ts, int l16, RecRegs<GATE> &R) {
+#pragma unroll
+    for (int q = 0; q < PER_SLOT; ++q) {
+        const int r = hi - 1 - (PER_SLOT * ts + q);
+        if (r >= lo) {
+            R.k[q] = *(const uint4 *)(a.rec_k + (rbase + r) * D + 8 * l16);
+            R.u[q] = *(const uint4 *)(a.rec_u + (rbase + r) * D + 8 * l16);
+            if (GATE) R.a[q] = *(const uint4 *)(a.rec_a + (rbase + r) * D + 8 * l16);
+            else R.as[q] = h2f(a.rec_a[rbase + r]);
+        }
+    }
+}
+
 template <int GATE, int CODE>
 __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     constexpr int G = GATE ? D : 1;     // decay values per record
@@ -53,9 +83,14 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     __shared__ float s_w[2][D];          // c . Gamma_{1:i} . x
     __shared__ float s_y[2][D];          // Gamma_{1:i} . x
     __shared__ float s_z[2][D];          // quantized-residual readout
-    __shared__ float s_P[CHUNK][G];      // Gamma_{j+1:i} of the records in this pass
-    __shared__ float s_red[CHUNK][2][D]; // per-group partial readouts
     __shared__ float s_kq[2];            // k~_t . q_t (per wave pair)
+    __shared__ union {
+        struct {
+            float bp[SLOTS][G];          // decay product of each slot's block
+            float pre[SLOTS][G];         // decay of everything newer than the block
+        } scan;
+        float red[SLOTS][2][D];          // per-slot partial readouts
+    } u_;
 
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -70,110 +105,157 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         return;
     }
 
-    // ---- issue the code loads first: 4 rows x 16 bytes per thread --------------
-    const int g8 = tid & 7;              // 16-channel key segment
-    const int rg = tid >> 3;             // rows rg, rg+32, rg+64, rg+96
+    const int l16 = tid & 15;            // 8-channel key segment / 8-value segment
+    const int ts = tid >> 4;             // slot 0..15
+    const int g8 = tid & 7;              // 16-channel key segment of the code rows
+    const int rg = tid >> 3;             // code rows rg, rg+32, rg+64, rg+96
+    const size_t rbase = (size_t)tile * a.window;
+
+    // ---- issue every load of the tile -----------------------------------------
     const uint8_t *zt = a.codes + (size_t)tile * D * D;
     uint4 zr[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) zr[m] = *(const uint4 *)(zt + (size_t)(rg + 32 * m) * D + 16 * g8);
+    float dlt[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (g8 == 0) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) dlt[m] = a.scale[tvec + rg + 32 * m];
+    }
+    uint4 ck = make_uint4(0, 0, 0, 0), cu = make_uint4(0, 0, 0, 0);
+    if (ts < a.n_comp) {
+        const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
+        ck = *(const uint4 *)(a.comp_k + cb);
+        cu = *(const uint4 *)(a.comp_u + cb);
+    }
+    RecRegs<GATE> R;
+    int hi = n, lo = n > PASS ? n - PASS : 0;
+    load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
 
     // ---- token inputs, this token's record -------------------------------------
-    float carry = 1.0f;                  // running Gamma_{j+1:i} (channel tid, or scalar)
+    // carry: decay of every record newer than the current pass, channel tid
+    // (the scalar gate keeps the same product in every thread below D)
+    float carry = 1.0f;
+    float cs = 0.0f;
     if (tid < D) {
         const float kx = a.k[kvec + tid];
         const float qx = a.q[kvec + tid];
+        cs = a.smooth[tvec + tid];
         s_x[0][tid] = kx;
         s_x[1][tid] = qx;
         const float al = GATE ? a.alpha[tvec + tid] : a.alpha[tile];
         const uint16_t ah = f2h(al);
         carry = h2f(ah);
-        const size_t slot = (size_t)tile * a.window + n;
+        const size_t slot = rbase + n;
         if (GATE) a.rec_a[slot * D + tid] = ah;
         else if (tid == 0) a.rec_a[slot] = ah;
         const uint16_t tkh = f2h(a.beta[tile] * kx);         // k~_t = fp16(beta_t k_t)
         a.rec_k[slot * D + tid] = tkh;
-        float kq = wave_sum(h2f(tkh) * qx);
+        const float kq = wave_sum(h2f(tkh) * qx);
         if ((tid & 63) == 0) s_kq[tid >> 6] = kq;
     }
-    __syncthreads();
 
-    // ---- buffered records, newest first, CHUNK per pass -------------------------
-    const int l16 = tid & 15;            // 8-channel key segment / 8-value segment
-    const int ts = tid >> 4;             // term slot 0..15
-    float xk[8], xq[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        xk[j] = s_x[0][8 * l16 + j];
-        xq[j] = s_x[1][8 * l16 + j];
-    }
     float acc_k[8], acc_q[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc_k[j] = acc_q[j] = 0.0f;
 
-    const size_t rbase = (size_t)tile * a.window;
-    for (int hi = n; hi > 0; hi -= CHUNK) {
-        const int lo = hi > CHUNK ? hi - CHUNK : 0;
-        // suffix decays of records lo..hi-1: P_r = prod of alpha over records r+1..n-1 and token i
-        if (tid < D) {
-            for (int r = hi - 1; r >= lo; --r) {
-                if (GATE) {
-                    s_P[r - lo][tid] = carry;
-                    carry *= h2f(a.rec_a[(rbase + r) * D + tid]);
-                } else {
-                    if (tid == 0) s_P[r - lo][0] = carry;
-                    carry *= h2f(a.rec_a[rbase + r]);
+    // ---- buffered records, newest first, up to PASS per pass ----------------------
+    if (n > 0) {
+        bool first = true;
+        float xk[8], xq[8];
+        while (true) {
+            // decay product of this slot's block, per channel of its segment
+            float bp[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) bp[j] = 1.0f;
+#pragma unroll
+            for (int q = 0; q < PER_SLOT; ++q) {
+                if (hi - 1 - (PER_SLOT * ts + q) >= lo) {
+                    if (GATE) {
+                        float av[8];
+                        unpack_h8(R.a[q], av);
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) bp[j] *= av[j];
+                    } else {
+                        bp[0] *= R.as[q];
+                    }
                 }
             }
-        }
-        __syncthreads();
-        const int r = lo + ts;
-        if (r < hi) {
-            const uint4 kp = *(const uint4 *)(a.rec_k + (rbase + r) * D + 8 * l16);
-            const uint4 up = *(const uint4 *)(a.rec_u + (rbase + r) * D + 8 * l16);
-            float kv[8], uv[8];
-            unpack_h8(kp, kv);
-            unpack_h8(up, uv);
-            float pk = 0.0f, pq = 0.0f;
             if (GATE) {
 #pragma unroll
+                for (int j = 0; j < 8; ++j) u_.scan.bp[ts][8 * l16 + j] = bp[j];
+            } else if (l16 == 0) {
+                u_.scan.bp[ts][0] = bp[0];
+            }
+            __syncthreads();
+            if (first) {
+#pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const float t = kv[j] * s_P[ts][(8 * l16 + j) % G];
+                    xk[j] = s_x[0][8 * l16 + j];
+                    xq[j] = s_x[1][8 * l16 + j];
+                }
+                first = false;
+            }
+            // exclusive scan over the slots; slot 0 holds the newest block
+            if (tid < D) {
+                const int ch = GATE ? tid : 0;
+                float c = carry;
+#pragma unroll
+                for (int s = 0; s < SLOTS; ++s) {
+                    if (GATE || tid == 0) u_.scan.pre[s][ch] = c;
+                    c *= u_.scan.bp[s][ch];
+                }
+                carry = c;
+            }
+            __syncthreads();
+            float P[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) P[j] = u_.scan.pre[ts][GATE ? 8 * l16 + j : 0];
+#pragma unroll
+            for (int q = 0; q < PER_SLOT; ++q) {
+                if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                float kv[8], uv[8];
+                unpack_h8(R.k[q], kv);
+                unpack_h8(R.u[q], uv);
+                float pk = 0.0f, pq = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float t = kv[j] * P[j];
                     pk = fmaf(t, xk[j], pk);
                     pq = fmaf(t, xq[j], pq);
                 }
-            } else {
+                pk = row16_sum(pk);
+                pq = row16_sum(pq);
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    pk = fmaf(kv[j], xk[j], pk);
-                    pq = fmaf(kv[j], xq[j], pq);
+                    acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
+                    acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+                }
+                if (GATE) {
+                    float av[8];
+                    unpack_h8(R.a[q], av);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) P[j] *= av[j];
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) P[j] *= R.as[q];
                 }
             }
-            pk = row16_sum(pk);
-            pq = row16_sum(pq);
-            if (!GATE) {
-                const float p = s_P[ts][0];
-                pk *= p;
-                pq *= p;
-            }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
-                acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
-            }
+            if (lo == 0) break;
+            // older records: another pass (scalar gate with W > 64 only).  The
+            // next pass's first barrier orders these scan reads before its writes.
+            hi = lo;
+            lo = hi > PASS ? hi - PASS : 0;
+            load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
         }
-        __syncthreads();
     }
 
     // ---- carry is now Gamma_{1:i}: base and token read vectors -------------------
     if (tid < D) {
-        const float c = a.smooth[tvec + tid];
-        const float gm = carry;      // scalar gate: every thread < D carries the same product
-        const float yk = gm * s_x[0][tid], yq = gm * s_x[1][tid];
+        const float yk = carry * s_x[0][tid], yq = carry * s_x[1][tid];
         s_y[0][tid] = yk;
         s_y[1][tid] = yq;
-        s_w[0][tid] = c * yk;
-        s_w[1][tid] = c * yq;
+        s_w[0][tid] = cs * yk;
+        s_w[1][tid] = cs * yq;
     }
     __syncthreads();
 
@@ -199,21 +281,17 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             pq = row8_sum(pq);
             if (g8 == 0) {
                 const int vrow = rg + 32 * m;
-                const float dv = a.scale[tvec + vrow];
-                s_z[0][vrow] = dv * pk;
-                s_z[1][vrow] = dv * pq;
+                s_z[0][vrow] = dlt[m] * pk;
+                s_z[1][vrow] = dlt[m] * pq;
             }
         }
     }
 
     // ---- Compensator Tokens: token ts, same decay as the base -------------------
     if (ts < a.n_comp) {
-        const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
-        const uint4 kp = *(const uint4 *)(a.comp_k + cb);
-        const uint4 up = *(const uint4 *)(a.comp_u + cb);
         float kv[8], uv[8];
-        unpack_h8(kp, kv);
-        unpack_h8(up, uv);
+        unpack_h8(ck, kv);
+        unpack_h8(cu, uv);
         float pk = 0.0f, pq = 0.0f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -228,10 +306,11 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
         }
     }
+    // the scan buffers are dead since the barrier above; reuse them
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        s_red[ts][0][8 * l16 + j] = acc_k[j];
-        s_red[ts][1][8 * l16 + j] = acc_q[j];
+        u_.red[ts][0][8 * l16 + j] = acc_k[j];
+        u_.red[ts][1][8 * l16 + j] = acc_q[j];
     }
     __syncthreads();
 
@@ -239,9 +318,9 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     if (tid < D) {
         float ak = s_z[0][tid], aq = s_z[1][tid];
 #pragma unroll
-        for (int s = 0; s < CHUNK; ++s) {
-            ak += s_red[s][0][tid];
-            aq += s_red[s][1][tid];
+        for (int s = 0; s < SLOTS; ++s) {
+            ak += u_.red[s][0][tid];
+            aq += u_.red[s][1][tid];
         }
         const uint16_t uh = f2h(a.v[tvec + tid] - ak);     // u_t = fp16(v_t - A^T k_t)
         a.rec_u[(rbase + n) * D + tid] = uh;
