@@ -49,6 +49,7 @@ struct DecodeArgs {
     int group;      // heads_v / heads_k
     int window;
     int n_comp;
+    int tiles;
 };
 
 template <int GATE>
@@ -98,20 +99,22 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     const size_t kvec = ((size_t)b * (a.heads_v / a.group) + hv / a.group) * D;
     const size_t tvec = (size_t)tile * D;
 
-    const int n = a.rec_len[tile];
-    if (n >= a.window || n < 0) {        // window buffer full (or corrupt): tile untouched
-        if (tid == 0) atomicOr(a.err, n < 0 ? (int)LQ_DEVERR_BAD_REC_LEN : (int)LQ_DEVERR_WINDOW_FULL);
-        if (tid < D) a.o[tvec + tid] = __builtin_nanf("");
-        return;
-    }
-
     const int l16 = tid & 15;            // 8-channel key segment / 8-value segment
     const int ts = tid >> 4;             // slot 0..15
     const int g8 = tid & 7;              // 16-channel key segment of the code rows
     const int rg = tid >> 3;             // code rows rg, rg+32, rg+64, rg+96
     const size_t rbase = (size_t)tile * a.window;
 
-    // ---- issue every load of the tile -----------------------------------------
+    // ---- issue every load of the tile: first what does not depend on rec_len ----
+    float kx = 0.0f, qx = 0.0f, cs = 0.0f, al = 0.0f, vx = 0.0f, bt = 0.0f;
+    if (tid < D) {
+        kx = a.k[kvec + tid];
+        qx = a.q[kvec + tid];
+        cs = a.smooth[tvec + tid];
+        al = GATE ? a.alpha[tvec + tid] : a.alpha[tile];
+        vx = a.v[tvec + tid];
+        bt = a.beta[tile];
+    }
     const uint8_t *zt = a.codes + (size_t)tile * D * D;
     uint4 zr[4];
 #pragma unroll
@@ -127,6 +130,12 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         ck = *(const uint4 *)(a.comp_k + cb);
         cu = *(const uint4 *)(a.comp_u + cb);
     }
+    const int n = a.rec_len[tile];
+    if (n >= a.window || n < 0) {        // window buffer full (or corrupt): tile untouched
+        if (tid == 0) atomicOr(a.err, n < 0 ? (int)LQ_DEVERR_BAD_REC_LEN : (int)LQ_DEVERR_WINDOW_FULL);
+        if (tid < D) a.o[tvec + tid] = __builtin_nanf("");
+        return;
+    }
     RecRegs<GATE> R;
     int hi = n, lo = n > PASS ? n - PASS : 0;
     load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
@@ -135,20 +144,15 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     // carry: decay of every record newer than the current pass, channel tid
     // (the scalar gate keeps the same product in every thread below D)
     float carry = 1.0f;
-    float cs = 0.0f;
     if (tid < D) {
-        const float kx = a.k[kvec + tid];
-        const float qx = a.q[kvec + tid];
-        cs = a.smooth[tvec + tid];
         s_x[0][tid] = kx;
         s_x[1][tid] = qx;
-        const float al = GATE ? a.alpha[tvec + tid] : a.alpha[tile];
         const uint16_t ah = f2h(al);
         carry = h2f(ah);
         const size_t slot = rbase + n;
         if (GATE) a.rec_a[slot * D + tid] = ah;
         else if (tid == 0) a.rec_a[slot] = ah;
-        const uint16_t tkh = f2h(a.beta[tile] * kx);         // k~_t = fp16(beta_t k_t)
+        const uint16_t tkh = f2h(bt * kx);                   // k~_t = fp16(beta_t k_t)
         a.rec_k[slot * D + tid] = tkh;
         const float kq = wave_sum(h2f(tkh) * qx);
         if ((tid & 63) == 0) s_kq[tid >> 6] = kq;
@@ -213,13 +217,15 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
 #pragma unroll
             for (int q = 0; q < PER_SLOT; ++q) {
                 if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                // products with an FP16 operand are written as fma(h, x, 0), which
+                // takes the half directly (same value as the product)
                 float kv[8], uv[8];
                 unpack_h8(R.k[q], kv);
                 unpack_h8(R.u[q], uv);
                 float pk = 0.0f, pq = 0.0f;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const float t = kv[j] * P[j];
+                    const float t = fmaf(kv[j], P[j], 0.0f);
                     pk = fmaf(t, xk[j], pk);
                     pq = fmaf(t, xq[j], pq);
                 }
@@ -234,7 +240,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
                     float av[8];
                     unpack_h8(R.a[q], av);
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) P[j] *= av[j];
+                    for (int j = 0; j < 8; ++j) P[j] = fmaf(av[j], P[j], 0.0f);
                 } else {
 #pragma unroll
                     for (int j = 0; j < 8; ++j) P[j] *= R.as[q];
@@ -322,7 +328,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             ak += u_.red[s][0][tid];
             aq += u_.red[s][1][tid];
         }
-        const uint16_t uh = f2h(a.v[tvec + tid] - ak);     // u_t = fp16(v_t - A^T k_t)
+        const uint16_t uh = f2h(vx - ak);                  // u_t = fp16(v_t - A^T k_t)
         a.rec_u[(rbase + n) * D + tid] = uh;
         a.o[tvec + tid] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
         if (tid == 0) a.rec_len[tile] = n + 1;
@@ -330,8 +336,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
 }
 
 template <int GATE, int CODE>
-hipError_t launch(const DecodeArgs &args, int tiles, hipStream_t st) {
-    hipLaunchKernelGGL((decode_kernel<GATE, CODE>), dim3(tiles), dim3(NT), 0, st, args);
+hipError_t launch(const DecodeArgs &args, hipStream_t st) {
+    hipLaunchKernelGGL((decode_kernel<GATE, CODE>), dim3(args.tiles), dim3(NT), 0, st, args);
     return hipGetLastError();
 }
 
@@ -359,10 +365,10 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
     a.group = d.heads_v / d.heads_k;
     a.window = d.window;
     a.n_comp = d.n_comp;
-    const int tiles = d.batch * d.heads_v;
+    a.tiles = d.batch * d.heads_v;
     if (d.gate == LQ_GATE_DIAG)
-        return d.code == LQ_CODE_E4M3 ? launch<1, 1>(a, tiles, st) : launch<1, 0>(a, tiles, st);
-    return d.code == LQ_CODE_E4M3 ? launch<0, 1>(a, tiles, st) : launch<0, 0>(a, tiles, st);
+        return d.code == LQ_CODE_E4M3 ? launch<1, 1>(a, st) : launch<1, 0>(a, st);
+    return d.code == LQ_CODE_E4M3 ? launch<0, 1>(a, st) : launch<0, 0>(a, st);
 }
 
 }  // namespace lq

@@ -1,10 +1,10 @@
 // Whole-tile kernels: quantize a given state, commit a window, dequantize.
 //
-// One 256-thread workgroup owns one 128 x 128 tile held in registers: thread
-// (kb, vb) keeps the 8 x 8 block M[8kb .. 8kb+7][8vb .. 8vb+7] of the state in
-// paper orientation (row = key channel).  kb is the lane's column inside its
-// 16-lane DPP row, so reductions over key channels are DPP row reductions;
-// reductions over value channels go through LDS.
+// One 256-thread workgroup (4 waves) owns one 128 x 128 tile held in
+// registers: thread (kb, vb) keeps the 8 x 8 block M[8kb .. 8kb+7][8vb .. 8vb+7]
+// of the state in paper orientation (row = key channel).  kb is the lane's
+// column inside its 16-lane DPP row, so reductions over key channels are DPP
+// row reductions; reductions over value channels go through LDS.
 //
 //   commit   : reconstruct S_p = Gamma_{1:p}[C dequant(Z) + K~ U~^T]
 //              + sum_j Gamma_{j+1:p} k~_j u_j^T  (Sec. 3.4 Eq. (smooth)),
@@ -15,8 +15,8 @@
 //
 // Quantization (Sec. 3.3 Eq. (compensator-rank-r), Sec. 3.4, App. B.3): r
 // Compensator Tokens fitted one after another by power iteration on the
-// deflated residual (start: key-row l2 norms; each sweep y = M^T x, x = M y,
-// x *= 1/|x|), each rounded to FP16 before it is subtracted; then the smoothing
+// deflated residual (start: key-row l2 norms; each sweep y = M^T x, x = M y;
+// the direction is normalised), each rounded to FP16 before it is subtracted; then the smoothing
 // scales c_k = sqrt(max(mean_v |R_kv|, 1e-12)), the per-value-channel scale
 // delta_v = max_k |R_kv / c_k| / qmax and the codes.
 //
@@ -35,6 +35,16 @@ namespace lq {
 namespace {
 
 constexpr int TCH = 16;     // rank-one records staged per pass
+constexpr int TT = 256;     // threads per tile
+constexpr int NVB = 16;     // value blocks
+constexpr int VPT = 8;      // value channels per thread
+
+// Per-key-channel vectors in LDS are stored swizzled: channel 8kb+a sits at
+// position 16a+kb, so the 16 lanes of a DPP row (kb = 0..15) touch 16
+// consecutive 8-byte words and never share a bank.  A thread t < 128 that
+// works on "position t" works on channel KCH(t).
+__device__ __forceinline__ constexpr int KP(int kb, int a) { return 16 * a + kb; }
+__device__ __forceinline__ constexpr int KCH(int t) { return 8 * (t & 15) + (t >> 4); }
 
 struct TileArgs {
     uint8_t *codes;
@@ -58,29 +68,40 @@ struct TileArgs {
 };
 
 struct TileShared {
-    double part[16][D];     // per-value-block partials of a sum over value channels
+    union {
+        double part[NVB][D];    // per-value-block partials of a sum over value channels
+        double pre[TCH][D];     // record staging: decay of every newer record
+    };
     double vec[D];          // broadcast vector
     double nrm[2];          // per-wave partial squared norms
     double key[TCH][D];     // staged record keys, decay folded in
     float val[TCH][D];      // staged record values
+    float bp[TCH][D];       // record staging: decay of each record
+    double tot[D];          // record staging: decay of a whole pass
 };
 
-// Sum p[a] (channel 8kb+a, this thread's value block) over the 16 value blocks;
-// thread t < 128 returns the sum for channel t.
+// Sum p[a] (channel 8kb+a, this thread's value block) over the 16 value
+// blocks through LDS; thread t < 128 returns the sum for channel KCH(t).
 __device__ __forceinline__ double reduce_over_values(TileShared &sh, const double *p, int kb, int vb) {
 #pragma unroll
-    for (int a = 0; a < 8; ++a) sh.part[vb][8 * kb + a] = p[a];
+    for (int a = 0; a < 8; ++a) sh.part[vb][KP(kb, a)] = p[a];
     __syncthreads();
     double s = 0.0;
     const int t = threadIdx.x;
     if (t < D) {
+        double v[NVB];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) s += sh.part[j][t];
+        for (int j = 0; j < NVB; ++j) v[j] = sh.part[j][t];
+#pragma unroll
+        for (int w = NVB / 2; w >= 1; w /= 2)
+#pragma unroll
+            for (int j = 0; j < w; ++j) v[j] += v[j + w];
+        s = v[0];
     }
     return s;
 }
 
-// Threads t < 128 publish x (channel t); after the barrier every thread reads
+// Threads t < 128 publish x (channel KCH(t)); after the barrier every thread reads
 // its 8 channels into xa and gets the squared norm of the whole vector.  The
 // barrier also ends every read of sh.part issued before the call.
 __device__ __forceinline__ double publish_vector(TileShared &sh, double x, double *xa, int kb) {
@@ -92,34 +113,61 @@ __device__ __forceinline__ double publish_vector(TileShared &sh, double x, doubl
     }
     __syncthreads();
 #pragma unroll
-    for (int a = 0; a < 8; ++a) xa[a] = sh.vec[8 * kb + a];
+    for (int a = 0; a < 8; ++a) xa[a] = sh.vec[KP(kb, a)];
     return sh.nrm[0] + sh.nrm[1];
 }
 
+// publish_vector without the norm.
+__device__ __forceinline__ void publish_only(TileShared &sh, double x, double *xa, int kb) {
+    const int t = threadIdx.x;
+    if (t < D) sh.vec[t] = x;
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < 8; ++a) xa[a] = sh.vec[KP(kb, a)];
+}
+
 template <int GATE, int CODE, int MODE>
-__global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
+__global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
     __shared__ TileShared sh;
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int kb = lane & 15;                       // key block  (DPP column)
-    const int vb = (tid >> 6) * 4 + (lane >> 4);    // value block
+    const int kb = lane & 15;                       // key block of 8 channels (DPP column)
+    const int vb = tid >> 4;                        // value block of VPT channels (0..15)
     const size_t tvec = (size_t)tile * D;
     const int r = A.n_comp;
 
-    double m[8][8];                                 // m[a][b] = M[8kb+a][8vb+b]
+    double m[8][VPT];                               // m[a][b] = M[8kb+a][VPT*vb+b]
 
     if (MODE == TILE_QUANTIZE) {
         const float *S = A.S_in + (size_t)tile * D * D;
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            const float4 *row = (const float4 *)(S + (size_t)(8 * vb + b) * D + 8 * kb);
+        for (int b = 0; b < VPT; ++b) {
+            const float4 *row = (const float4 *)(S + (size_t)(VPT * vb + b) * D + 8 * kb);
             const float4 lo = row[0], hi = row[1];
             m[0][b] = lo.x; m[1][b] = lo.y; m[2][b] = lo.z; m[3][b] = lo.w;
             m[4][b] = hi.x; m[5][b] = hi.y; m[6][b] = hi.z; m[7][b] = hi.w;
         }
     } else {
+        // Every global load of the reconstruction is issued here, ahead of
+        // its first use: rec_len, the codes and scales of this thread's
+        // block, the compensators (one 16-byte segment per thread) and the
+        // first pass of records.
         const int p = A.rec_len[tile];
+        const int l16 = tid & 15, ts = tid >> 4;    // staging: segment, slot
+        const uint8_t *zt = A.codes + (size_t)tile * D * D;
+        uint2 zp[VPT];
+#pragma unroll
+        for (int b = 0; b < VPT; ++b) zp[b] = *(const uint2 *)(zt + (size_t)(VPT * vb + b) * D + 8 * kb);
+        const float4 dl0 = *(const float4 *)(A.scale + tvec + VPT * vb);
+        const float4 dl1 = *(const float4 *)(A.scale + tvec + VPT * vb + 4);
+        const float4 c0 = *(const float4 *)(A.smooth + tvec + 8 * kb);
+        const float4 c1 = *(const float4 *)(A.smooth + tvec + 8 * kb + 4);
+        uint4 ck = make_uint4(0, 0, 0, 0), cu = ck;
+        if (ts < r) {
+            ck = *(const uint4 *)(A.comp_k + ((size_t)tile * r + ts) * D + 8 * l16);
+            cu = *(const uint4 *)(A.comp_u + ((size_t)tile * r + ts) * D + 8 * l16);
+        }
         if (p < 0 || p > A.window) {                                  // corrupt: tile untouched
             if (tid == 0) atomicOr(A.err, (int)LQ_DEVERR_BAD_REC_LEN);
             return;
@@ -128,88 +176,144 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
             const int req = tile / A.heads_v;
             if (p == 0 || (A.mask && A.mask[req] == 0)) return;   // uniform: tile untouched
         }
-#pragma unroll
-        for (int a = 0; a < 8; ++a)
-#pragma unroll
-            for (int b = 0; b < 8; ++b) m[a][b] = 0.0;
-
-        // records, newest first: k~_j . Gamma_{j+1:p} staged in LDS, TCH per pass
+        // records in passes of TCH, oldest pass first; slot ts of a pass takes
+        // record lo+ts, lane l16 its 8-channel / 8-value segment.
         const size_t rbase = (size_t)tile * A.window;
-        double carry = 1.0;                         // running Gamma_{j+1:p}, channel tid
-        for (int hi = p; hi > 0; hi -= TCH) {
-            const int lo = hi > TCH ? hi - TCH : 0;
-            if (tid < D) {
-                for (int j = hi - 1; j >= lo; --j) {
-                    sh.key[j - lo][tid] = carry * (double)h2f(A.rec_k[(rbase + j) * D + tid]);
-                    sh.val[j - lo][tid] = h2f(A.rec_u[(rbase + j) * D + tid]);
-                    carry *= (double)(GATE ? h2f(A.rec_a[(rbase + j) * D + tid])
-                                           : h2f(A.rec_a[rbase + j]));
+        uint4 rk = make_uint4(0, 0, 0, 0), ru = rk, ra = rk;
+        auto load_pass = [&](int lo_, int hi_) {
+            const int rr = lo_ + ts;
+            if (rr < hi_) {
+                rk = *(const uint4 *)(A.rec_k + (rbase + rr) * D + 8 * l16);
+                ru = *(const uint4 *)(A.rec_u + (rbase + rr) * D + 8 * l16);
+                if (GATE) ra = *(const uint4 *)(A.rec_a + (rbase + rr) * D + 8 * l16);
+                else ra.x = A.rec_a[rbase + rr];
+            }
+        };
+        if (p > 0) load_pass(0, p < TCH ? p : TCH);
+
+        // window-start base C dequant(Z) (Sec. 3.4 Eq. (smooth))
+        {
+            const float dv[8] = {dl0.x, dl0.y, dl0.z, dl0.w, dl1.x, dl1.y, dl1.z, dl1.w};
+            const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+            for (int a = 0; a < 8; ++a) {
+#pragma unroll
+                for (int b = 0; b < VPT; ++b) {
+                    const uint32_t w = a < 4 ? zp[b].x : zp[b].y;
+                    const uint32_t z = (w >> (8 * (a & 3))) & 0xFFu;
+                    const double zf = CODE ? (double)e4m3_to_f<0>(z) : (double)(int8_t)(uint8_t)z;
+                    m[a][b] = (double)cv[a] * (zf * (double)dv[b]);
                 }
             }
+        }
+        // + its compensators K~ U~^T
+        if (ts < r) {
+            float kv[8], uv[8];
+            unpack_h8(ck, kv);
+            unpack_h8(cu, uv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                sh.key[ts][KP(l16, j)] = (double)kv[j];
+                sh.val[ts][8 * l16 + j] = uv[j];
+            }
+        }
+        __syncthreads();
+#pragma unroll 1
+        for (int h = 0; h < r; ++h) {
+            double kd[8], ud[VPT];
+#pragma unroll
+            for (int a = 0; a < 8; ++a) kd[a] = sh.key[h][KP(kb, a)];
+#pragma unroll
+            for (int b = 0; b < VPT; ++b) ud[b] = (double)sh.val[h][VPT * vb + b];
+#pragma unroll
+            for (int a = 0; a < 8; ++a)
+#pragma unroll
+                for (int b = 0; b < VPT; ++b) m[a][b] = fma(kd[a], ud[b], m[a][b]);
+        }
+        __syncthreads();
+
+        // Each pass: m <- Gamma_pass * m + sum_j Gamma_{j+1:hi} k~_j u_j^T, the
+        // window recursion taken TCH records at a time; within the pass the
+        // decay of every later record is an exclusive suffix product.
+        for (int lo = 0; lo < p; lo += TCH) {
+            const int hi = lo + TCH < p ? lo + TCH : p;
+            const bool mine = lo + ts < hi;
+            float av[8], kv[8], uv[8];
+            unpack_h8(ra, av);
+            unpack_h8(rk, kv);
+            unpack_h8(ru, uv);
+            if (!GATE) av[0] = h2f((uint16_t)ra.x);
+            if (GATE) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sh.bp[ts][KP(l16, j)] = mine ? av[j] : 1.0f;
+            } else if (l16 == 0) {
+                sh.bp[ts][0] = mine ? av[0] : 1.0f;
+            }
             __syncthreads();
-            for (int j = 0; j < hi - lo; ++j) {
-                double kv[8], uv[8];
+            if (tid < D) {
+                const int ch = GATE ? tid : 0;
+                float bv[TCH];
 #pragma unroll
-                for (int a = 0; a < 8; ++a) kv[a] = sh.key[j][8 * kb + a];
+                for (int sl = 0; sl < TCH; ++sl) bv[sl] = sh.bp[sl][ch];
+                double c = 1.0;
 #pragma unroll
-                for (int b = 0; b < 8; ++b) uv[b] = (double)sh.val[j][8 * vb + b];
+                for (int sl = TCH - 1; sl >= 0; --sl) {
+                    if (GATE || tid == 0) sh.pre[sl][ch] = c;
+                    c *= (double)bv[sl];
+                }
+                if (GATE || tid == 0) sh.tot[ch] = c;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const double P = sh.pre[ts][GATE ? KP(l16, j) : 0];
+                sh.key[ts][KP(l16, j)] = mine ? P * (double)kv[j] : 0.0;
+                sh.val[ts][8 * l16 + j] = mine ? uv[j] : 0.0f;
+            }
+#pragma unroll
+            for (int a = 0; a < 8; ++a) {
+                const double T = sh.tot[GATE ? KP(kb, a) : 0];
+#pragma unroll
+                for (int b = 0; b < VPT; ++b) m[a][b] *= T;
+            }
+            if (hi < p) load_pass(hi, hi + TCH < p ? hi + TCH : p);
+            __syncthreads();
+            // records two at a time (a pass holds zeros past its last record),
+            // so one record's LDS reads overlap the other's FMAs
+            const int nrec = hi - lo;
+#pragma unroll 1
+            for (int j = 0; j < nrec; j += 2) {
+                double k0[8], k1[8], u0[VPT], u1[VPT];
+#pragma unroll
+                for (int a = 0; a < 8; ++a) k0[a] = sh.key[j][KP(kb, a)];
+#pragma unroll
+                for (int b = 0; b < VPT; ++b) u0[b] = (double)sh.val[j][VPT * vb + b];
+#pragma unroll
+                for (int a = 0; a < 8; ++a) k1[a] = sh.key[j + 1][KP(kb, a)];
+#pragma unroll
+                for (int b = 0; b < VPT; ++b) u1[b] = (double)sh.val[j + 1][VPT * vb + b];
 #pragma unroll
                 for (int a = 0; a < 8; ++a)
 #pragma unroll
-                    for (int b = 0; b < 8; ++b) m[a][b] = fma(kv[a], uv[b], m[a][b]);
+                    for (int b = 0; b < VPT; ++b) m[a][b] = fma(k0[a], u0[b], m[a][b]);
+#pragma unroll
+                for (int a = 0; a < 8; ++a)
+#pragma unroll
+                    for (int b = 0; b < VPT; ++b) m[a][b] = fma(k1[a], u1[b], m[a][b]);
             }
             __syncthreads();
-        }
-        // carry = Gamma_{1:p}: decay of the window-start base and its tokens.
-        // Stage the tokens in LDS (r <= TCH); publish_vector's barrier covers it.
-        if (tid < D) {
-            for (int h = 0; h < r; ++h) {
-                sh.key[h][tid] = (double)h2f(A.comp_k[((size_t)tile * r + h) * D + tid]);
-                sh.val[h][tid] = h2f(A.comp_u[((size_t)tile * r + h) * D + tid]);
-            }
-        }
-        double ga[8];
-        publish_vector(sh, carry, ga, kb);
-        double cs[8], dl[8];
-#pragma unroll
-        for (int a = 0; a < 8; ++a) cs[a] = (double)A.smooth[tvec + 8 * kb + a];
-#pragma unroll
-        for (int b = 0; b < 8; ++b) dl[b] = (double)A.scale[tvec + 8 * vb + b];
-        const uint8_t *zt = A.codes + (size_t)tile * D * D;
-        uint2 zp[8];
-#pragma unroll
-        for (int b = 0; b < 8; ++b) zp[b] = *(const uint2 *)(zt + (size_t)(8 * vb + b) * D + 8 * kb);
-        // base + tokens, one key channel at a time so only 8 extra fp64 values are live
-#pragma unroll
-        for (int a = 0; a < 8; ++a) {
-            double base[8];
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const uint32_t w = a < 4 ? zp[b].x : zp[b].y;
-                const uint32_t z = (w >> (8 * (a & 3))) & 0xFFu;
-                const double zf = CODE ? (double)e4m3_to_f<0>(z) : (double)(int8_t)(uint8_t)z;
-                base[b] = cs[a] * (zf * dl[b]);
-            }
-            for (int h = 0; h < r; ++h) {
-                const double kh = sh.key[h][8 * kb + a];
-#pragma unroll
-                for (int b = 0; b < 8; ++b) base[b] = fma(kh, (double)sh.val[h][8 * vb + b], base[b]);
-            }
-#pragma unroll
-            for (int b = 0; b < 8; ++b) m[a][b] = fma(ga[a], base[b], m[a][b]);
         }
 
         if (MODE == TILE_DEQUANT) {
             float *S = A.S_out + (size_t)tile * D * D;
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                float4 *row = (float4 *)(S + (size_t)(8 * vb + b) * D + 8 * kb);
+            for (int b = 0; b < VPT; ++b) {
+                float4 *row = (float4 *)(S + (size_t)(VPT * vb + b) * D + 8 * kb);
                 row[0] = make_float4((float)m[0][b], (float)m[1][b], (float)m[2][b], (float)m[3][b]);
                 row[1] = make_float4((float)m[4][b], (float)m[5][b], (float)m[6][b], (float)m[7][b]);
             }
             return;
         }
-        __syncthreads();    // every read of sh.vec above is done before it is reused
     }
 
     // ------------------------------------------------------------------ quantize
@@ -220,7 +324,7 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
         for (int a = 0; a < 8; ++a) {
             double s = 0.0;
 #pragma unroll
-            for (int b = 0; b < 8; ++b) s = fma(m[a][b], m[a][b], s);
+            for (int b = 0; b < VPT; ++b) s = fma(m[a][b], m[a][b], s);
             p8[a] = s;
         }
         double x = sqrt(reduce_over_values(sh, p8, kb, vb));
@@ -231,42 +335,50 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
 #pragma unroll
             for (int a = 0; a < 8; ++a) xa[a] *= inv;
         }
+        // Sweeps without per-sweep normalisation: each sweep is scaled by the
+        // power of two sc ~ 1/|M|_F^2 (exact, so only the direction matters)
+        // and the vector is normalised once after the last sweep.  A sweep
+        // grows the norm by at most sc*sigma_1^2 < 2.
+        const double sc = ok ? ldexp(1.0, -ilogb(nrm * nrm)) : 0.0;
         for (int it = 0; ok && it < A.power_iters; ++it) {
-            double y[8];
+            double y[VPT];
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
+            for (int b = 0; b < VPT; ++b) {
                 double s = 0.0;
 #pragma unroll
                 for (int a = 0; a < 8; ++a) s = fma(m[a][b], xa[a], s);
-                y[b] = row16_sum(s);                // y_v = sum_k M_kv x_k
+                y[b] = row16_sum(s) * sc;           // y_v = sc * sum_k M_kv x_k
             }
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
                 double s = 0.0;
 #pragma unroll
-                for (int b = 0; b < 8; ++b) s = fma(m[a][b], y[b], s);
+                for (int b = 0; b < VPT; ++b) s = fma(m[a][b], y[b], s);
                 p8[a] = s;
             }
-            x = reduce_over_values(sh, p8, kb, vb);  // x_k = sum_v M_kv y_v
-            nrm = sqrt(publish_vector(sh, x, xa, kb));
-            if (!(nrm > 0.0)) {
-                ok = false;
-                break;
-            }
-            const double inv = 1.0 / nrm;
+            x = reduce_over_values(sh, p8, kb, vb);      // x_k = sum_v M_kv y_v
+            if (it + 1 < A.power_iters) {
+                publish_only(sh, x, xa, kb);
+            } else {
+                nrm = sqrt(publish_vector(sh, x, xa, kb));
+                ok = nrm > 0.0;
+                if (ok) {
+                    const double inv = 1.0 / nrm;
 #pragma unroll
-            for (int a = 0; a < 8; ++a) xa[a] *= inv;
+                    for (int a = 0; a < 8; ++a) xa[a] *= inv;
+                }
+            }
         }
-        uint16_t kh[8], uh[8];
+        uint16_t kh[8], uh[VPT];
         if (ok) {
-            double kf[8], uf[8];
+            double kf[8], uf[VPT];
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
                 kh[a] = d2h_via_f32(xa[a]);          // rounded through fp32
                 kf[a] = (double)h2f(kh[a]);
             }
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
+            for (int b = 0; b < VPT; ++b) {
                 double s = 0.0;
 #pragma unroll
                 for (int a = 0; a < 8; ++a) s = fma(m[a][b], kf[a], s);
@@ -276,10 +388,12 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
 #pragma unroll
             for (int a = 0; a < 8; ++a)
 #pragma unroll
-                for (int b = 0; b < 8; ++b) m[a][b] = fma(-kf[a], uf[b], m[a][b]);
+                for (int b = 0; b < VPT; ++b) m[a][b] = fma(-kf[a], uf[b], m[a][b]);
         } else {
 #pragma unroll
-            for (int a = 0; a < 8; ++a) kh[a] = uh[a] = 0;
+            for (int a = 0; a < 8; ++a) kh[a] = 0;
+#pragma unroll
+            for (int b = 0; b < VPT; ++b) uh[b] = 0;
         }
         if (vb == 0) {
             uint4 w;
@@ -295,7 +409,7 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
             w.y = uh[2] | ((uint32_t)uh[3] << 16);
             w.z = uh[4] | ((uint32_t)uh[5] << 16);
             w.w = uh[6] | ((uint32_t)uh[7] << 16);
-            *(uint4 *)(A.comp_u + ((size_t)tile * r + h) * D + 8 * vb) = w;
+            *(uint4 *)(A.comp_u + ((size_t)tile * r + h) * D + VPT * vb) = w;
         }
     }
 
@@ -307,13 +421,13 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
         for (int a = 0; a < 8; ++a) {
             double s = 0.0;
 #pragma unroll
-            for (int b = 0; b < 8; ++b) s += fabs(m[a][b]);
+            for (int b = 0; b < VPT; ++b) s += fabs(m[a][b]);
             p8[a] = s;
         }
         const double s = reduce_over_values(sh, p8, kb, vb);
         float c = 1.0f;
         if (A.smooth_on) c = (float)sqrt(fmax(s * (1.0 / (double)D), (double)1e-12f));
-        if (tid < D) A.smooth[tvec + tid] = c;
+        if (tid < D) A.smooth[tvec + KCH(tid)] = c;
         publish_vector(sh, (double)c, csd, kb);
     }
     // per-value-channel scale and codes, decided in fp32
@@ -323,7 +437,7 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
     for (int a = 0; a < 8; ++a) ic[a] = 1.0f / (float)csd[a];
     uint8_t *zt = A.codes + (size_t)tile * D * D;
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
+    for (int b = 0; b < VPT; ++b) {
         float rc[8];
         float amax = 0.0f;
 #pragma unroll
@@ -348,15 +462,15 @@ __global__ __launch_bounds__(NT) void tile_kernel(TileArgs A) {
             if (a < 4) w0 |= code << (8 * a);
             else w1 |= code << (8 * (a - 4));
         }
-        *(uint2 *)(zt + (size_t)(8 * vb + b) * D + 8 * kb) = make_uint2(w0, w1);
-        if (kb == 0) A.scale[tvec + 8 * vb + b] = dl;
+        *(uint2 *)(zt + (size_t)(VPT * vb + b) * D + 8 * kb) = make_uint2(w0, w1);
+        if (kb == 0) A.scale[tvec + VPT * vb + b] = dl;
     }
     if (tid == 0) A.rec_len[tile] = 0;
 }
 
 template <int GATE, int CODE, int MODE>
 hipError_t launch3(const TileArgs &a, int tiles, hipStream_t st) {
-    hipLaunchKernelGGL((tile_kernel<GATE, CODE, MODE>), dim3(tiles), dim3(NT), 0, st, a);
+    hipLaunchKernelGGL((tile_kernel<GATE, CODE, MODE>), dim3(tiles), dim3(TT), 0, st, a);
     return hipGetLastError();
 }
 
