@@ -9,14 +9,15 @@
 // output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
 //
-// Every global load of the tile is issued before the first barrier: the
-// d_v x d_k code bytes (16-byte loads, 8 lanes per 128-byte row), the token
-// pairs and up to 64 records (16 slots of 16 lanes, each slot a contiguous
-// block of 4 records, 16 bytes of key, correction and decay per lane).  The
-// decays Gamma_{j+1:i} are products of the FP16 record decays: each slot forms
-// the product of its block, one scan over the 16 slots gives every block the
-// decay of all newer records, and the slot walks its block from the newest
-// record back.  No d_k x d_v intermediate exists.
+// Every global load of the tile is issued before the first barrier, those that
+// do not depend on rec_len first: the token inputs, the d_v x d_k code bytes
+// (16-byte loads, 8 lanes per 128-byte row), the compensators, then rec_len and
+// one pass of records (16 slots of 16 lanes, each slot a contiguous block of
+// records, 16 bytes of key, correction and decay per lane).  The decays
+// Gamma_{j+1:i} are products of the FP16 record decays: each slot forms the
+// product of its block, one scan over the 16 slots gives every block the decay
+// of all newer records, and the slot walks its block from the newest record
+// back.  No d_k x d_v intermediate exists.
 #include "lq_device.hpp"
 #include "lq_internal.hpp"
 
@@ -25,8 +26,13 @@ namespace lq {
 namespace {
 
 constexpr int SLOTS = 16;            // 16-lane groups per workgroup
-constexpr int PER_SLOT = 4;          // records per slot and pass
-constexpr int PASS = SLOTS * PER_SLOT;
+// Records per slot and pass: the diagonal gate carries a 16-byte decay per lane
+// and record, so it holds two per slot (32 per pass) to stay at 4 resident
+// workgroups per CU; the scalar gate holds four (64 per pass).
+template <int GATE> struct Pass {
+    static constexpr int PER_SLOT = GATE ? 2 : 4;
+    static constexpr int N = SLOTS * PER_SLOT;
+};
 
 struct DecodeArgs {
     const uint8_t *codes;
@@ -54,6 +60,7 @@ struct DecodeArgs {
 
 template <int GATE>
 struct RecRegs {
+    static constexpr int PER_SLOT = Pass<GATE>::PER_SLOT;
     uint4 k[PER_SLOT];               // FP16 keys, 8 channels
     uint4 u[PER_SLOT];               // FP16 corrections, 8 values
     uint4 a[GATE ? PER_SLOT : 1];    // FP16 decays, 8 channels (diagonal gate)
@@ -65,6 +72,7 @@ struct RecRegs {
 template <int GATE>
 __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi,
                                              int ts, int l16, RecRegs<GATE> &R) {
+    constexpr int PER_SLOT = Pass<GATE>::PER_SLOT;
 #pragma unroll
     for (int q = 0; q < PER_SLOT; ++q) {
         const int r = hi - 1 - (PER_SLOT * ts + q);
@@ -137,6 +145,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         return;
     }
     RecRegs<GATE> R;
+    constexpr int PER_SLOT = Pass<GATE>::PER_SLOT, PASS = Pass<GATE>::N;
     int hi = n, lo = n > PASS ? n - PASS : 0;
     load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
 
