@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
     ap.add_argument("--no-baselines", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tiles", type=int, default=1024)
+    ap.add_argument("--cpu-sample-tiles", type=int, default=8192)
     ap.add_argument("--profile", action="store_true",
                     help="short run for profilers: setup, warmup and the timed steps only")
     return ap.parse_args()
@@ -204,39 +204,93 @@ def time_steps(fn, steps, warmup):
     return e0.elapsed_time(e1) / 1e3, wall
 
 
-def per_launch_times(wl, dims, S0, toks):
-    """HIP-event durations of every decode launch of one window (all positions),
-    of the commit that ends it and of the window-start quantization, measured
-    on the stream the kernels run on."""
+def per_launch_times(wl, dims, S0, toks, reps=3):
+    """Average kernel durations, measured with HIP events on the stream the
+    kernels run on: the decode launches of one whole window (positions 1..W)
+    replayed as one graph, divided by W; the commit that ends the window; the
+    window-start quantization."""
     import torch
     from paper_2609_38166_amd import binding as B_
     st = B_.State.empty(dims)
     o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
     q, k, v, a, b = toks
     W = wl.window
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(W + 2)]
-    res = {"decode": [], "commit": [], "quantize": []}
-    for rep in range(3):
-        ev[0][0].record()
-        B_.leapquant_quantize_state(dims, S0, st)
-        ev[0][1].record()
+
+    def window():
         for i in range(W):
-            ev[i + 1][0].record()
             B_.leapquant_decode_step(dims, st, q[i], k[i], v[i], a[i], b[i], o)
-            ev[i + 1][1].record()
-        ev[W + 1][0].record()
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        B_.leapquant_quantize_state(dims, S0, st)
+        window()
         B_.leapquant_window_commit(dims, st)
-        ev[W + 1][1].record()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        window()
+    torch.cuda.synchronize()
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+    res = {"decode": [], "commit": [], "quantize": []}
+    for rep in range(reps + 1):
+        e = [ev() for _ in range(6)]
+        e[0].record()
+        B_.leapquant_quantize_state(dims, S0, st)
+        e[1].record()
+        e[2].record()
+        g.replay()
+        e[3].record()
+        e[4].record()
+        B_.leapquant_window_commit(dims, st)
+        e[5].record()
         torch.cuda.synchronize()
         if rep == 0:
             continue                      # first pass warms caches and clocks
-        res["quantize"].append(ev[0][0].elapsed_time(ev[0][1]))
-        res["decode"].append([ev[i + 1][0].elapsed_time(ev[i + 1][1]) for i in range(W)])
-        res["commit"].append(ev[W + 1][0].elapsed_time(ev[W + 1][1]))
-    dec = np.mean(np.array(res["decode"]), axis=0)   # ms per position
-    return {"decode_ms_by_pos": dec, "decode_ms": float(dec.mean()),
-            "commit_ms": float(np.mean(res["commit"])), "quantize_ms": float(np.mean(res["quantize"]))}
+        res["quantize"].append(e[0].elapsed_time(e[1]))
+        res["decode"].append(e[2].elapsed_time(e[3]) / W)
+        res["commit"].append(e[4].elapsed_time(e[5]))
+    bits = B_.leapquant_check_error(st)
+    if bits:
+        raise RuntimeError(f"device error bits {bits} during the per-launch timing")
+    return {k_: float(np.mean(v_)) for k_, v_ in (("decode_ms", res["decode"]),
+                                                   ("commit_ms", res["commit"]),
+                                                   ("quantize_ms", res["quantize"]))}
+
+
+def copy_calibration(nbytes=1 << 30):
+    """One plain device-to-device copy of known size, for scaling the HBM byte
+    counters of a profiler run (FETCH_SIZE / WRITE_SIZE of this dispatch are
+    compared with nbytes read and nbytes written)."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def traffic_from_profile(wl):
+    """HBM bytes per decode launch from the committed counter summary, if it
+    was taken on the current decode kernel source; None otherwise."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"decode_step_traffic_{wl.name}.md")
+    src = os.path.join(ROOT, "paper_2609_38166_amd", "csrc", "lq_decode.hip")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            key, val = line[2:].split(":", 1)
+            fields[key.strip()] = val.strip().strip("`")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if fields.get("lq_decode.hip sha256") != sha or "traffic bytes per launch" not in fields:
+        return None
+    return float(fields["traffic bytes per launch"])
 
 
 def cpu_baseline(wl, n_tiles):
@@ -290,11 +344,15 @@ def main():
     runner = Runner(wl, dims, S0, toks, use_graph=not args.no_graph)
     log("[bench] runner ready")
     secs, wall = time_steps(runner.step, args.steps, args.warmup)
+    bits = B_.leapquant_check_error(runner.st)
+    if bits:
+        raise RuntimeError(f"device error bits {bits} after the timed steps")
     ms_step = secs / args.steps * 1e3
     tile_steps = wl.tiles * wl.steps
     value = tile_steps * args.steps / secs
     log(f"[bench] leapquant {ms_step:.3f} ms/step, {value:.4g} token-head steps/s")
     if args.profile:
+        copy_calibration()
         print(json.dumps({"profile_ms_per_step": ms_step}), flush=True)
         return
 
@@ -308,6 +366,7 @@ def main():
     eff = step_bytes / (ms_step * 1e-3) / 1e9
     log(f"[bench] decode {kt['decode_ms'] * 1e3:.1f} us/launch ({achieved:.0f} GB/s), "
         f"commit {kt['commit_ms'] * 1e3:.1f} us, quantize {kt['quantize_ms'] * 1e3:.1f} us")
+    traffic = traffic_from_profile(wl)
 
     out = {
         "metric": "token-head decode steps/s + effective HBM GB/s (% of peak), speedup vs bf16 state",
@@ -326,11 +385,9 @@ def main():
         "frac_of_hbm_peak": round(eff / PEAK_HBM_GBS, 4),
         "roofline": {"kernel": "decode_step", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                     "traffic": None,
+                     "traffic": None if traffic is None else round(traffic),
                      "bytes_per_launch": round(dec_avg_bytes), "avg_launch_us": round(kt["decode_ms"] * 1e3, 2)},
         "kernels_us": {"decode_avg": round(kt["decode_ms"] * 1e3, 2),
-                       "decode_first_pos": round(float(kt["decode_ms_by_pos"][0]) * 1e3, 2),
-                       "decode_last_pos": round(float(kt["decode_ms_by_pos"][-1]) * 1e3, 2),
                        "commit": round(kt["commit_ms"] * 1e3, 2),
                        "quantize": round(kt["quantize_ms"] * 1e3, 2)},
     }
