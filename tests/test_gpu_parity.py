@@ -350,3 +350,54 @@ def test_decode_is_deterministic():
         res.append((torch.stack(outs), st.codes.clone(), st.comp_u.clone(), st.rec_u.clone()))
     for a, b in zip(res[0], res[1]):
         assert torch.equal(a, b)
+
+
+# --------------------------------------------------------------------------- full sizes
+
+FULL = {
+    "kda_kimi": (W_["kda_kimi"], 32, 1),
+    "gdn_qwen3next_int8": (W_["gdn_qwen3next"], 32, 1),
+    "gdn_qwen3next_e4m3": (W_["gdn_qwen3next"].with_(name="gdn_qwen3next_e4m3", code=synth.CODE_E4M3), 32, 1),
+    "gdn_stress": (W_["gdn_stress"], 48, 2),
+    "gdn_long": (W_["gdn_long"], 24, 1),
+}
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_full_size_window_parity(name):
+    """Every launch at the workload's full size (all tiles, as benchmarked); the
+    oracle checks a seeded tile sample (outlier tiles included where only a
+    fraction has them).  gdn_long has W = 128, so its decode takes two record
+    passes."""
+    wl, n, windows = FULL[name]
+    H.sampled_window_parity(wl, n_sample=n, n_windows=windows)
+
+
+def test_full_size_bulk_quantize_parity():
+    """leapquant_quantize_state over all 262144 cached states (17.2 GB fp32 in
+    HBM); the oracle quantizes a seeded sample of them."""
+    wl = W_["bulk_quantize"]
+    dims = H.gdims(wl)
+    cfg = H.ocfg(wl)
+    vt = H.sample_tiles(wl, 32)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(wl.seed)
+    S = torch.randn((wl.batch, wl.heads_v, wl.dv, wl.dk), device="cuda", generator=g)
+    Ss = np.stack([synth.bulk_states(wl, 1, first=int(t))[0] for t in vt])     # [n][dv][dk]
+    S.view(wl.tiles, wl.dv, wl.dk)[torch.as_tensor(vt, device="cuda")] = H.dev(Ss)
+    st = B.State.empty(dims)
+    B.leapquant_quantize_state(dims, S, st)
+    got = H.download_rep(st, vt)
+    del S
+    exp = {"Z": [], "delta": [], "c": [], "Kt": [], "Ut": []}
+    for i in range(len(vt)):
+        rep = O.quantize(cfg, Ss[i].T.astype(np.float64))
+        for k_ in exp:
+            exp[k_].append(getattr(rep, k_))
+    exp = {k_: np.stack(v_) for k_, v_ in exp.items()}
+    cr = H.compare_rep(cfg, got, exp, wl.code)
+    H.log(f"[bulk_quantize] full size: {cr}")
+    assert cr["code_eq"] >= 0.999 and cr["code_maxdiff"] <= 1, cr
+    assert cr["deq_rel"] <= 1e-3 and cr.get("comp_rel", 0.0) <= 1e-3, cr
+    assert cr["delta_rel"] <= 1e-5 and cr["c_rel"] <= 1e-5, cr
+    assert np.all(got["rec_len"] == 0)
