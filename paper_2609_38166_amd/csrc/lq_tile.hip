@@ -78,6 +78,7 @@ struct TileShared {
     float val[TCH][D];      // staged record values
     float bp[TCH][D];       // record staging: decay of each record
     double tot[D];          // record staging: decay of a whole pass
+    double rowp[NVB][8 * 17];   // per-row partials of sums over key blocks (row_sum8)
 };
 
 // Sum p[a] (channel 8kb+a, this thread's value block) over the 16 value
@@ -115,6 +116,33 @@ __device__ __forceinline__ double publish_vector(TileShared &sh, double x, doubl
 #pragma unroll
     for (int a = 0; a < 8; ++a) xa[a] = sh.vec[KP(kb, a)];
     return sh.nrm[0] + sh.nrm[1];
+}
+
+// Sum v[b] (b = 0..7, this thread's value channels) over the 16 key blocks
+// of its DPP row and return the 8 sums, times `scale`, in v.  The row's 16
+// lanes belong to one wave, so a row-private LDS region needs no workgroup
+// barrier: lane kb stores its partials at [b][kb] (rows of 17 words, so the
+// 8 channels a read touches sit in distinct banks, and consecutive rows start
+// 16 banks apart), lane kb then sums channel kb & 7 over the 16 lanes and
+// parks the sum in the row's spare word, which every lane reads back.
+__device__ __forceinline__ void row_sum8(TileShared &sh, double *v, int kb, int vb, double scale) {
+    double *r = sh.rowp[vb];
+#pragma unroll
+    for (int b = 0; b < 8; ++b) r[17 * b + kb] = v[b];
+    __builtin_amdgcn_wave_barrier();
+    const int c = kb & 7;
+    double t[16];
+#pragma unroll
+    for (int l = 0; l < 16; ++l) t[l] = r[17 * c + l];
+#pragma unroll
+    for (int w = 8; w >= 1; w /= 2)
+#pragma unroll
+        for (int l = 0; l < w; ++l) t[l] += t[l + w];
+    if (kb < 8) r[17 * c + 16] = t[0] * scale;
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int b = 0; b < 8; ++b) v[b] = r[17 * b + 16];
+    __builtin_amdgcn_wave_barrier();
 }
 
 // publish_vector without the norm.
@@ -347,8 +375,9 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
                 double s = 0.0;
 #pragma unroll
                 for (int a = 0; a < 8; ++a) s = fma(m[a][b], xa[a], s);
-                y[b] = row16_sum(s) * sc;           // y_v = sc * sum_k M_kv x_k
+                y[b] = s;
             }
+            row_sum8(sh, y, kb, vb, sc);            // y_v = sc * sum_k M_kv x_k
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
                 double s = 0.0;
@@ -377,12 +406,18 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
                 kh[a] = d2h_via_f32(xa[a]);          // rounded through fp32
                 kf[a] = (double)h2f(kh[a]);
             }
+            double us[VPT];
 #pragma unroll
             for (int b = 0; b < VPT; ++b) {
                 double s = 0.0;
 #pragma unroll
                 for (int a = 0; a < 8; ++a) s = fma(m[a][b], kf[a], s);
-                uh[b] = d2h_via_f32(row16_sum(s));   // u~_v = fp16(sum_k M_kv k~_k)
+                us[b] = s;
+            }
+            row_sum8(sh, us, kb, vb, 1.0);
+#pragma unroll
+            for (int b = 0; b < VPT; ++b) {
+                uh[b] = d2h_via_f32(us[b]);          // u~_v = fp16(sum_k M_kv k~_k)
                 uf[b] = (double)h2f(uh[b]);
             }
 #pragma unroll
