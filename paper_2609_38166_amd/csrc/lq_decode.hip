@@ -211,48 +211,72 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             // exclusive scan over the slots; slot 0 holds the newest block
             if (tid < D) {
                 const int ch = GATE ? tid : 0;
+                float bv[SLOTS];
+#pragma unroll
+                for (int s = 0; s < SLOTS; ++s) bv[s] = u_.scan.bp[s][ch];
                 float c = carry;
 #pragma unroll
                 for (int s = 0; s < SLOTS; ++s) {
                     if (GATE || tid == 0) u_.scan.pre[s][ch] = c;
-                    c *= u_.scan.bp[s][ch];
+                    c *= bv[s];
                 }
                 carry = c;
             }
             __syncthreads();
-            float P[8];
+            if (GATE) {
+                float P[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) P[j] = u_.scan.pre[ts][GATE ? 8 * l16 + j : 0];
+                for (int j = 0; j < 8; ++j) P[j] = u_.scan.pre[ts][8 * l16 + j];
 #pragma unroll
-            for (int q = 0; q < PER_SLOT; ++q) {
-                if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
-                // products with an FP16 operand are written as fma(h, x, 0), which
-                // takes the half directly (same value as the product)
-                float kv[8], uv[8];
-                unpack_h8(R.k[q], kv);
-                unpack_h8(R.u[q], uv);
-                float pk = 0.0f, pq = 0.0f;
+                for (int q = 0; q < PER_SLOT; ++q) {
+                    if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                    // products with an FP16 operand are written as fma(h, x, 0), which
+                    // takes the half directly (same value as the product)
+                    float kv[8], uv[8];
+                    unpack_h8(R.k[q], kv);
+                    unpack_h8(R.u[q], uv);
+                    float pk = 0.0f, pq = 0.0f;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const float t = fmaf(kv[j], P[j], 0.0f);
-                    pk = fmaf(t, xk[j], pk);
-                    pq = fmaf(t, xq[j], pq);
-                }
-                pk = row16_sum(pk);
-                pq = row16_sum(pq);
+                    for (int j = 0; j < 8; ++j) {
+                        const float t = fmaf(kv[j], P[j], 0.0f);
+                        pk = fmaf(t, xk[j], pk);
+                        pq = fmaf(t, xq[j], pq);
+                    }
+                    pk = row16_sum(pk);
+                    pq = row16_sum(pq);
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
-                    acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
-                }
-                if (GATE) {
+                    for (int j = 0; j < 8; ++j) {
+                        acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
+                        acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+                    }
                     float av[8];
                     unpack_h8(R.a[q], av);
 #pragma unroll
                     for (int j = 0; j < 8; ++j) P[j] = fmaf(av[j], P[j], 0.0f);
-                } else {
+                }
+            } else {
+                // scalar decay: one product per slot, applied to the two dot products
+                float P = u_.scan.pre[ts][0];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) P[j] *= R.as[q];
+                for (int q = 0; q < PER_SLOT; ++q) {
+                    if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                    float kv[8], uv[8];
+                    unpack_h8(R.k[q], kv);
+                    unpack_h8(R.u[q], uv);
+                    float pk = 0.0f, pq = 0.0f;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        pk = fmaf(kv[j], xk[j], pk);
+                        pq = fmaf(kv[j], xq[j], pq);
+                    }
+                    pk = row16_sum(pk) * P;
+                    pq = row16_sum(pq) * P;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
+                        acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+                    }
+                    P *= R.as[q];
                 }
             }
             if (lo == 0) break;
