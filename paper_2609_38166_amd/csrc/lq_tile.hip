@@ -74,11 +74,15 @@ struct TileShared {
     };
     double vec[D];          // broadcast vector
     double nrm[2];          // per-wave partial squared norms
-    double key[TCH][D];     // staged record keys, decay folded in
-    float val[TCH][D];      // staged record values
-    float bp[TCH][D];       // record staging: decay of each record
-    double tot[D];          // record staging: decay of a whole pass
-    double rowp[NVB][8 * 17];   // per-row partials of sums over key blocks (row_sum8)
+    union {
+        struct {            // reconstruction phase
+            double key[TCH][D];     // staged record keys, decay folded in
+            float val[TCH][D];      // staged record values
+            float bp[TCH][D];       // decay of each staged record
+            double tot[D];          // decay of a whole pass
+        };
+        double rowp[NVB][8 * 17];   // fit phase: per-row partials of sums over key blocks
+    };
 };
 
 // Sum p[a] (channel 8kb+a, this thread's value block) over the 16 value
