@@ -54,6 +54,8 @@ extern "C" {
 #define LQ_GATE_DIAG   1     /* KDA: D_t = Diag(alpha_t), alpha_t in R^{d_k}          */
 #define LQ_CODE_INT8   0     /* symmetric INT8, dequant = code * delta_v, |code|<=127 */
 #define LQ_CODE_E4M3   1     /* OCP FP8 E4M3FN codes, dequant = e4m3(code) * delta_v  */
+#define LQ_CODE_INT4   2     /* symmetric 4-bit, |code| <= 7, two codes per byte      */
+#define LQ_CODE_INT6   3     /* symmetric 6-bit, |code| <= 31, four codes per 3 bytes  */
 #define LQ_STATE_F32   0     /* baseline state in fp32                               */
 #define LQ_STATE_BF16  1     /* baseline state in bf16, rounded to nearest even      */
 
@@ -77,14 +79,20 @@ typedef struct {
     int32_t n_comp;      /* r in [0, 16]: Compensator Tokens per tile                */
     int32_t power_iters; /* power-iteration sweeps per token, >= 1 when r > 0        */
     int32_t gate;        /* LQ_GATE_SCALAR or LQ_GATE_DIAG                            */
-    int32_t code;        /* LQ_CODE_INT8 or LQ_CODE_E4M3                             */
+    int32_t code;        /* LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4 or LQ_CODE_INT6  */
     int32_t smooth;      /* 1: residual smoothing (Sec. 3.4); 0: c = 1               */
 } lq_dims;
 
 /* The quantized state of all tiles (device pointers, caller-owned).
  * Sizes per tile; g = 1 for the scalar gate, g = d_k for the diagonal gate. */
 typedef struct {
-    void     *codes;   /* [d_v][d_k] bytes: int8 two's complement or E4M3FN        */
+    void     *codes;   /* [d_v][d_k*b/8] bytes, b = 8, 8, 4, 6 bits per code:
+                        *   INT8: one two's-complement byte per key channel;
+                        *   E4M3: one E4M3FN byte per key channel;
+                        *   INT4: byte i holds channel 2i (low nibble) and 2i+1
+                        *         (high nibble), two's complement;
+                        *   INT6: bytes 3i..3i+2, read little-endian as 24 bits,
+                        *         hold channels 4i..4i+3 at bits 6q..6q+5       */
     float    *scale;   /* [d_v]  delta_v = max_k |R^C_kv| / 127 (INT8) or / 448    */
     float    *smooth;  /* [d_k]  c_k, the residual smoothing scale                 */
     uint16_t *comp_k;  /* [r][d_k] fp16 key vectors k~_h of the Compensator Tokens */
@@ -117,6 +125,8 @@ int32_t leapquant_state_bytes(const lq_dims *dims, size_t bytes_out[10]);
  * token is rounded to FP16 before it is subtracted, so the codes absorb that
  * rounding.  c_k = sqrt(max(mean_v |R_kv|, 1e-12)), R^C = R * (1/c_k),
  * delta_v = max_k |R^C_kv| / 127, code = clamp(rint(R^C * 127/max), +-127).
+ * The 6- and 4-bit variants (the paper's lower-bit LeapQuant, Sec. 4.1-4.2)
+ * use the same rule with qmax = 31 and 7 (2^(b-1) - 1) and packed storage.
  */
 int32_t leapquant_quantize_state(const lq_dims *dims, const float *S, lq_state *st, void *stream);
 

@@ -64,7 +64,7 @@ typedef struct {
     int32_t n_comp;        /* r: Compensator Tokens */
     int32_t power_iters;   /* power-iteration sweeps per token */
     int32_t gate;          /* 0: scalar decay (GDN); 1: per-key-channel decay (KDA) */
-    int32_t code;          /* 0: INT8 codes; 1: FP8 E4M3FN codes */
+    int32_t code;          /* 0: INT8; 1: FP8 E4M3FN; 2: INT4; 3: INT6 codes */
     int32_t smooth;        /* 1: residual smoothing; 0: c = 1 */
     int32_t quantize;      /* 1: quantize at window ends; 0: keep the state exact */
     int32_t round_records; /* 1: FP16 records (alpha, write key, correction); 0: exact */
@@ -76,10 +76,24 @@ enum { LQO_STATE_EXACT = 0, LQO_STATE_F32 = 1, LQO_STATE_BF16 = 2 };
 static real f16v(real x) { return (real)lqo_f16_to_f32(lqo_f32_to_f16((float)x)); }
 static real rec_round(const lqo_cfg *cfg, real x) { return cfg->round_records ? f16v(x) : x; }
 
+/* Codes are held one per byte here (the packing of 4- and 6-bit codes is a
+ * storage layout, not arithmetic): integer codes as two's-complement bytes,
+ * E4M3 codes as their bit pattern. */
 static real code_value(const lqo_cfg *cfg, uint8_t z)
 {
     if (cfg->code == 1) return (real)lqo_e4m3_to_f32(z);
     return (real)(int8_t)z;
+}
+
+/* Largest code magnitude: 2^(b-1) - 1 for b-bit symmetric integers, 448 for E4M3. */
+static float code_qmax(const lqo_cfg *cfg)
+{
+    switch (cfg->code) {
+    case 1: return 448.0f;
+    case 2: return 7.0f;
+    case 3: return 31.0f;
+    default: return 127.0f;
+    }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -103,6 +117,8 @@ static real code_value(const lqo_cfg *cfg, uint8_t z)
  * Codes (App. B.3): per value channel v, a_v = max_k |R^C_kv|.  INT8:
  * delta_v = a_v/127, code = clamp(rint(R^C_kv * (127/a_v)), -127, 127), ties to
  * even.  E4M3: delta_v = a_v/448, code = e4m3(clamp(R^C_kv * (448/a_v), +-448)).
+ * The 6- and 4-bit variants (Sec. 4.1, 4.2) read the same per-value-channel
+ * symmetric rule with qmax = 2^(b-1) - 1: 31 and 7.
  * A zero column gets delta_v = 0 and zero codes.  The code decision is taken in
  * fp32 from the fp32-rounded residual, as the GPU takes it.
  */
@@ -174,7 +190,7 @@ static void quantize_impl(const lqo_cfg *cfg, const double *S_in, uint8_t *Z, fl
     }
 
     /* per-value-channel symmetric codes, decided in fp32 */
-    const float qmax = cfg->code == 1 ? 448.0f : 127.0f;
+    const float qmax = code_qmax(cfg);
     for (int v = 0; v < dv; ++v) {
         float amax = 0.0f;
         for (int k = 0; k < dk; ++k) {
@@ -199,8 +215,8 @@ static void quantize_impl(const lqo_cfg *cfg, const double *S_in, uint8_t *Z, fl
                 Z[k * dv + v] = lqo_f32_to_e4m3(t);
             } else {
                 float q = rintf(t);
-                if (q > 127.0f) q = 127.0f;
-                if (q < -127.0f) q = -127.0f;
+                if (q > qmax) q = qmax;
+                if (q < -qmax) q = -qmax;
                 Z[k * dv + v] = (uint8_t)(int8_t)q;
             }
         }

@@ -50,7 +50,7 @@ class _Outputs(C.Structure):
 
 
 GATE_SCALAR, GATE_DIAG = 0, 1
-CODE_INT8, CODE_E4M3 = 0, 1
+CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6 = 0, 1, 2, 3
 STATE_EXACT, STATE_F32, STATE_BF16 = 0, 1, 2
 
 

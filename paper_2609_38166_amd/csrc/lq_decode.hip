@@ -10,8 +10,9 @@
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
 //
 // Every global load of the tile is issued before the first barrier, those that
-// do not depend on rec_len first: the token inputs, the d_v x d_k code bytes
-// (16-byte loads, 8 lanes per 128-byte row), the compensators, then rec_len and
+// do not depend on rec_len first: the token inputs, the d_v x d_k codes (16
+// codes per lane: 16, 12 or 8 bytes for 8-, 6- or 4-bit codes, 8 lanes per
+// row), the compensators, then rec_len and
 // one pass of records (16 slots of 16 lanes, each slot a contiguous block of
 // records, 16 bytes of key, correction and decay per lane).  The decays
 // Gamma_{j+1:i} are products of the FP16 record decays: each slot forms the
@@ -69,6 +70,18 @@ struct RecRegs {
 
 // Issue the loads of the records in [lo, hi) that belong to slot ts: record
 // hi-1-(PER_SLOT*ts+q) goes to register set q (newest first).
+// 16 consecutive codes of a row: 16 bytes (byte formats), 8 (INT4) or 12 (INT6).
+template <int CODE>
+__device__ __forceinline__ uint4 load_codes16(const uint8_t *p) {
+    if (CODE <= 1) return *(const uint4 *)p;
+    if (CODE == 2) {
+        const uint2 w = *(const uint2 *)p;
+        return make_uint4(w.x, w.y, 0u, 0u);
+    }
+    const uint32_t *w = (const uint32_t *)p;
+    return make_uint4(w[0], w[1], w[2], 0u);
+}
+
 template <int GATE>
 __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi,
                                              int ts, int l16, RecRegs<GATE> &R) {
@@ -123,10 +136,11 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         vx = a.v[tvec + tid];
         bt = a.beta[tile];
     }
-    const uint8_t *zt = a.codes + (size_t)tile * D * D;
+    constexpr int ROWB = D * CodeFmt<CODE>::BITS / 8;   // code bytes per value row
+    const uint8_t *zt = a.codes + (size_t)tile * D * ROWB;
     uint4 zr[4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) zr[m] = *(const uint4 *)(zt + (size_t)(rg + 32 * m) * D + 16 * g8);
+    for (int m = 0; m < 4; ++m) zr[m] = load_codes16<CODE>(zt + (size_t)(rg + 32 * m) * ROWB + 2 * CodeFmt<CODE>::BITS * g8);
     float dlt[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (g8 == 0) {
 #pragma unroll
@@ -211,14 +225,22 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             // exclusive scan over the slots; slot 0 holds the newest block
             if (tid < D) {
                 const int ch = GATE ? tid : 0;
-                float bv[SLOTS];
-#pragma unroll
-                for (int s = 0; s < SLOTS; ++s) bv[s] = u_.scan.bp[s][ch];
                 float c = carry;
+                if (GATE) {                  // slot products read ahead of the chain
+                    float bv[SLOTS];
 #pragma unroll
-                for (int s = 0; s < SLOTS; ++s) {
-                    if (GATE || tid == 0) u_.scan.pre[s][ch] = c;
-                    c *= bv[s];
+                    for (int s = 0; s < SLOTS; ++s) bv[s] = u_.scan.bp[s][ch];
+#pragma unroll
+                    for (int s = 0; s < SLOTS; ++s) {
+                        u_.scan.pre[s][ch] = c;
+                        c *= bv[s];
+                    }
+                } else {
+#pragma unroll
+                    for (int s = 0; s < SLOTS; ++s) {
+                        if (tid == 0) u_.scan.pre[s][0] = c;
+                        c *= u_.scan.bp[s][0];
+                    }
                 }
                 carry = c;
             }
@@ -399,9 +421,20 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
     a.window = d.window;
     a.n_comp = d.n_comp;
     a.tiles = d.batch * d.heads_v;
-    if (d.gate == LQ_GATE_DIAG)
-        return d.code == LQ_CODE_E4M3 ? launch<1, 1>(a, st) : launch<1, 0>(a, st);
-    return d.code == LQ_CODE_E4M3 ? launch<0, 1>(a, st) : launch<0, 0>(a, st);
+    if (d.gate == LQ_GATE_DIAG) {
+        switch (d.code) {
+            case LQ_CODE_E4M3: return launch<1, 1>(a, st);
+            case LQ_CODE_INT4: return launch<1, 2>(a, st);
+            case LQ_CODE_INT6: return launch<1, 3>(a, st);
+            default: return launch<1, 0>(a, st);
+        }
+    }
+    switch (d.code) {
+        case LQ_CODE_E4M3: return launch<0, 1>(a, st);
+        case LQ_CODE_INT4: return launch<0, 2>(a, st);
+        case LQ_CODE_INT6: return launch<0, 3>(a, st);
+        default: return launch<0, 0>(a, st);
+    }
 }
 
 }  // namespace lq

@@ -130,42 +130,76 @@ __device__ __forceinline__ uint8_t f_to_e4m3(float x) {
     return (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(x, x, 0, false) & 0xFF);
 }
 
+// ---- code formats -------------------------------------------------------------
+// CODE 0: INT8 byte; 1: E4M3FN byte; 2: INT4, two codes per byte (even channel in
+// the low nibble); 3: INT6, four codes per three bytes (channel 4i+q at bits
+// 6q..6q+5 of the little-endian 24-bit group i).  Codes are two's complement.
+template <int CODE> struct CodeFmt;
+template <> struct CodeFmt<0> { static constexpr int BITS = 8; static constexpr float QMAX = 127.0f; };
+template <> struct CodeFmt<1> { static constexpr int BITS = 8; static constexpr float QMAX = 448.0f; };
+template <> struct CodeFmt<2> { static constexpr int BITS = 4; static constexpr float QMAX = 7.0f; };
+template <> struct CodeFmt<3> { static constexpr int BITS = 6; static constexpr float QMAX = 31.0f; };
+
+// Signed field of `bits` bits at bit `off` of w (off + bits <= 32).
+__device__ __forceinline__ int32_t sfield(uint32_t w, int off, int bits) {
+    return (int32_t)(w << (32 - off - bits)) >> (32 - bits);
+}
+
+// Value of code j of a run of consecutive codes packed from bit 0 of the
+// little-endian words w[] (j, CODE compile-time after unrolling).
+template <int CODE>
+__device__ __forceinline__ float code_at(const uint32_t *w, int j) {
+    if (CODE == 0) return (float)sfield(w[j >> 2], 8 * (j & 3), 8);
+    if (CODE == 1) {
+        switch (j & 3) {
+            case 0: return e4m3_to_f<0>(w[j >> 2]);
+            case 1: return e4m3_to_f<1>(w[j >> 2]);
+            case 2: return e4m3_to_f<2>(w[j >> 2]);
+            default: return e4m3_to_f<3>(w[j >> 2]);
+        }
+    }
+    if (CODE == 2) return (float)sfield(w[j >> 3], 4 * (j & 7), 4);
+    const int bit = 6 * j, wi = bit >> 5, off = bit & 31;   // CODE == 3
+    if (off + 6 <= 32) return (float)sfield(w[wi], off, 6);
+    const uint32_t span = __builtin_amdgcn_alignbit(w[wi + 1], w[wi], off);
+    return (float)sfield(span, 0, 6);
+}
+
+// 16 consecutive codes (the first 4 * BITS / 8 words of p) to fp32.
 template <int CODE>
 __device__ __forceinline__ void decode16(const uint4 &p, float *f) {
     const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+    if (CODE == 0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        if (CODE == 0) {
+        for (int i = 0; i < 4; ++i) {
             f[4 * i + 0] = s8_to_f(w[i], 0);
             f[4 * i + 1] = s8_to_f(w[i], 1);
             f[4 * i + 2] = s8_to_f(w[i], 2);
             f[4 * i + 3] = s8_to_f(w[i], 3);
-        } else {
-            f[4 * i + 0] = e4m3_to_f<0>(w[i]);
-            f[4 * i + 1] = e4m3_to_f<1>(w[i]);
-            f[4 * i + 2] = e4m3_to_f<2>(w[i]);
-            f[4 * i + 3] = e4m3_to_f<3>(w[i]);
         }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) f[j] = code_at<CODE>(w, j);
     }
 }
 
+// Pack 8 codes (integers, or E4M3 bytes) into the words of their format.
 template <int CODE>
-__device__ __forceinline__ void decode8(const uint2 &p, float *f) {
-    const uint32_t w[2] = {p.x, p.y};
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        if (CODE == 0) {
-            f[4 * i + 0] = s8_to_f(w[i], 0);
-            f[4 * i + 1] = s8_to_f(w[i], 1);
-            f[4 * i + 2] = s8_to_f(w[i], 2);
-            f[4 * i + 3] = s8_to_f(w[i], 3);
-        } else {
-            f[4 * i + 0] = e4m3_to_f<0>(w[i]);
-            f[4 * i + 1] = e4m3_to_f<1>(w[i]);
-            f[4 * i + 2] = e4m3_to_f<2>(w[i]);
-            f[4 * i + 3] = e4m3_to_f<3>(w[i]);
-        }
+__device__ __forceinline__ uint2 encode8(const uint32_t *c) {
+    if (CODE <= 1) {
+        return make_uint2((c[0] & 0xFFu) | ((c[1] & 0xFFu) << 8) | ((c[2] & 0xFFu) << 16) | (c[3] << 24),
+                          (c[4] & 0xFFu) | ((c[5] & 0xFFu) << 8) | ((c[6] & 0xFFu) << 16) | (c[7] << 24));
     }
+    if (CODE == 2) {
+        uint32_t x = 0;
+#pragma unroll
+        for (int a = 0; a < 8; ++a) x |= (c[a] & 0xFu) << (4 * a);
+        return make_uint2(x, 0u);
+    }
+    uint64_t v = 0;                                          // CODE == 3: 48 bits
+#pragma unroll
+    for (int a = 0; a < 8; ++a) v |= (uint64_t)(c[a] & 0x3Fu) << (6 * a);
+    return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
 }
 
 // Non-temporal-free plain vector loads/stores through the vector memory path.

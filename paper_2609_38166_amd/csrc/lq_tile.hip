@@ -46,6 +46,34 @@ constexpr int VPT = 8;      // value channels per thread
 __device__ __forceinline__ constexpr int KP(int kb, int a) { return 16 * a + kb; }
 __device__ __forceinline__ constexpr int KCH(int t) { return 8 * (t & 15) + (t >> 4); }
 
+// The 8 codes of row v (value channel), key channels 8kb..8kb+7: 8 bytes for
+// the byte formats, 4 for INT4, 6 (three 16-bit words) for INT6.
+template <int CODE>
+__device__ __forceinline__ uint2 load_codes8(const uint8_t *codes, int tile, int v, int kb) {
+    constexpr int ROW = D * CodeFmt<CODE>::BITS / 8;
+    const uint8_t *p = codes + ((size_t)tile * D + v) * ROW + kb * CodeFmt<CODE>::BITS;
+    if (CODE <= 1) return *(const uint2 *)p;
+    if (CODE == 2) return make_uint2(*(const uint32_t *)p, 0u);
+    const uint16_t *h = (const uint16_t *)p;
+    return make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2]);
+}
+
+template <int CODE>
+__device__ __forceinline__ void store_codes8(uint8_t *codes, int tile, int v, int kb, uint2 w) {
+    constexpr int ROW = D * CodeFmt<CODE>::BITS / 8;
+    uint8_t *p = codes + ((size_t)tile * D + v) * ROW + kb * CodeFmt<CODE>::BITS;
+    if (CODE <= 1) {
+        *(uint2 *)p = w;
+    } else if (CODE == 2) {
+        *(uint32_t *)p = w.x;
+    } else {
+        uint16_t *h = (uint16_t *)p;
+        h[0] = (uint16_t)w.x;
+        h[1] = (uint16_t)(w.x >> 16);
+        h[2] = (uint16_t)w.y;
+    }
+}
+
 struct TileArgs {
     uint8_t *codes;
     float *scale;
@@ -187,10 +215,9 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
         // first pass of records.
         const int p = A.rec_len[tile];
         const int l16 = tid & 15, ts = tid >> 4;    // staging: segment, slot
-        const uint8_t *zt = A.codes + (size_t)tile * D * D;
         uint2 zp[VPT];
 #pragma unroll
-        for (int b = 0; b < VPT; ++b) zp[b] = *(const uint2 *)(zt + (size_t)(VPT * vb + b) * D + 8 * kb);
+        for (int b = 0; b < VPT; ++b) zp[b] = load_codes8<CODE>(A.codes, tile, VPT * vb + b, kb);
         const float4 dl0 = *(const float4 *)(A.scale + tvec + VPT * vb);
         const float4 dl1 = *(const float4 *)(A.scale + tvec + VPT * vb + 4);
         const float4 c0 = *(const float4 *)(A.smooth + tvec + 8 * kb);
@@ -231,9 +258,8 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
             for (int a = 0; a < 8; ++a) {
 #pragma unroll
                 for (int b = 0; b < VPT; ++b) {
-                    const uint32_t w = a < 4 ? zp[b].x : zp[b].y;
-                    const uint32_t z = (w >> (8 * (a & 3))) & 0xFFu;
-                    const double zf = CODE ? (double)e4m3_to_f<0>(z) : (double)(int8_t)(uint8_t)z;
+                    const uint32_t w[2] = {zp[b].x, zp[b].y};
+                    const double zf = (double)code_at<CODE>(w, a);
                     m[a][b] = (double)cv[a] * (zf * (double)dv[b]);
                 }
             }
@@ -470,11 +496,10 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
         publish_vector(sh, (double)c, csd, kb);
     }
     // per-value-channel scale and codes, decided in fp32
-    constexpr float QMAX = CODE ? 448.0f : 127.0f;
+    constexpr float QMAX = CodeFmt<CODE>::QMAX;
     float ic[8];
 #pragma unroll
     for (int a = 0; a < 8; ++a) ic[a] = 1.0f / (float)csd[a];
-    uint8_t *zt = A.codes + (size_t)tile * D * D;
 #pragma unroll
     for (int b = 0; b < VPT; ++b) {
         float rc[8];
@@ -487,21 +512,18 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
         amax = row16_max(amax);
         const float dl = amax > 0.0f ? amax / QMAX : 0.0f;
         const float inv = amax > 0.0f ? QMAX / amax : 0.0f;
-        uint32_t w0 = 0, w1 = 0;
+        uint32_t c8[8];
 #pragma unroll
         for (int a = 0; a < 8; ++a) {
-            uint32_t code;
-            if (CODE) {
-                const float t = fminf(fmaxf(rc[a] * inv, -448.0f), 448.0f);
-                code = f_to_e4m3(t);
+            if (CODE == 1) {
+                const float t = fminf(fmaxf(rc[a] * inv, -QMAX), QMAX);
+                c8[a] = f_to_e4m3(t);
             } else {
-                const float t = fminf(fmaxf(rintf(rc[a] * inv), -127.0f), 127.0f);
-                code = (uint32_t)(uint8_t)(int8_t)t;
+                const float t = fminf(fmaxf(rintf(rc[a] * inv), -QMAX), QMAX);
+                c8[a] = (uint32_t)(int32_t)t;
             }
-            if (a < 4) w0 |= code << (8 * a);
-            else w1 |= code << (8 * (a - 4));
         }
-        *(uint2 *)(zt + (size_t)(VPT * vb + b) * D + 8 * kb) = make_uint2(w0, w1);
+        store_codes8<CODE>(A.codes, tile, VPT * vb + b, kb, encode8<CODE>(c8));
         if (kb == 0) A.scale[tvec + VPT * vb + b] = dl;
     }
     if (tid == 0) A.rec_len[tile] = 0;
@@ -546,9 +568,20 @@ hipError_t launch_tile(const lq_dims &d, const StatePtrs &s, int mode, const flo
     a.power_iters = d.power_iters;
     a.smooth_on = d.smooth;
     const int tiles = d.batch * d.heads_v;
-    const bool kda = d.gate == LQ_GATE_DIAG, e4 = d.code == LQ_CODE_E4M3;
-    if (kda) return e4 ? launch2<1, 1>(a, tiles, mode, st) : launch2<1, 0>(a, tiles, mode, st);
-    return e4 ? launch2<0, 1>(a, tiles, mode, st) : launch2<0, 0>(a, tiles, mode, st);
+    if (d.gate == LQ_GATE_DIAG) {
+        switch (d.code) {
+            case LQ_CODE_E4M3: return launch2<1, 1>(a, tiles, mode, st);
+            case LQ_CODE_INT4: return launch2<1, 2>(a, tiles, mode, st);
+            case LQ_CODE_INT6: return launch2<1, 3>(a, tiles, mode, st);
+            default: return launch2<1, 0>(a, tiles, mode, st);
+        }
+    }
+    switch (d.code) {
+        case LQ_CODE_E4M3: return launch2<0, 1>(a, tiles, mode, st);
+        case LQ_CODE_INT4: return launch2<0, 2>(a, tiles, mode, st);
+        case LQ_CODE_INT6: return launch2<0, 3>(a, tiles, mode, st);
+        default: return launch2<0, 0>(a, tiles, mode, st);
+    }
 }
 
 }  // namespace lq

@@ -30,7 +30,7 @@ from dataclasses import dataclass, field, replace
 import numpy as np
 
 GATE_SCALAR, GATE_DIAG = 0, 1
-CODE_INT8, CODE_E4M3 = 0, 1
+CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6 = 0, 1, 2, 3
 PHASE_PREFILL, PHASE_DECODE, PHASE_OUTLIER = 0, 1, 2
 
 
@@ -79,6 +79,9 @@ WORKLOADS = {
     # 8192 cached prefix snapshots x 32 heads, quantized in bulk
     "bulk_quantize": Workload("bulk_quantize", 8192, 32, 32, 0, 1, 8, GATE_SCALAR, seed=20260005),
 }
+# the KDA layer with the lower-bit residual codes (same inputs, r = 8)
+WORKLOADS["kda_kimi_int4"] = WORKLOADS["kda_kimi"].with_(name="kda_kimi_int4", code=CODE_INT4)
+WORKLOADS["kda_kimi_int6"] = WORKLOADS["kda_kimi"].with_(name="kda_kimi_int6", code=CODE_INT6)
 
 
 def _threads(n=None) -> int:

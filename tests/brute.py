@@ -14,9 +14,9 @@ def f16(x):
     return np.float64(np.float16(np.float32(x)))
 
 
-def int8_codes_bruteforce(x32: float, delta32: float) -> int:
-    """Nearest code in [-127, 127] to x/delta (exhaustive), ties to even."""
-    cand = np.arange(-127, 128, dtype=np.float64)
+def int8_codes_bruteforce(x32: float, delta32: float, qmax: int = 127) -> int:
+    """Nearest code in [-qmax, qmax] to x/delta (exhaustive), ties to even."""
+    cand = np.arange(-qmax, qmax + 1, dtype=np.float64)
     target = np.float64(x32) / np.float64(delta32)
     d = np.abs(target - cand)
     best = np.flatnonzero(d == d.min())
@@ -26,8 +26,9 @@ def int8_codes_bruteforce(x32: float, delta32: float) -> int:
     return even[0]
 
 
-def quantize(S, r, iters, smooth=True):
-    """S: [dk][dv] float64.  Returns (Z int [dk][dv], delta f32 [dv], c f32 [dk], Kt, Ut)."""
+def quantize(S, r, iters, smooth=True, qmax=127):
+    """S: [dk][dv] float64.  Returns (Z int [dk][dv], delta f32 [dv], c f32 [dk], Kt, Ut).
+    qmax: largest integer code (127, 31 or 7 for 8-, 6- or 4-bit codes)."""
     dk, dv = S.shape
     M = S.astype(np.float64).copy()
     Kt = np.zeros((r, dk))
@@ -69,9 +70,9 @@ def quantize(S, r, iters, smooth=True):
         a = np.float32(np.max(np.abs(Rc[:, v])))
         if a == 0:
             continue
-        delta[v] = np.float32(a / np.float32(127.0))
+        delta[v] = np.float32(a / np.float32(qmax))
         for k in range(dk):
-            Z[k, v] = int8_codes_bruteforce(Rc[k, v], np.float64(a) / 127.0)
+            Z[k, v] = int8_codes_bruteforce(Rc[k, v], np.float64(a) / qmax, qmax)
     return Z, delta, c, Kt, Ut
 
 

@@ -70,7 +70,7 @@ def gdims(wl: synth.Workload, **kw) -> B.lq_dims:
 def code_ordinal(Z, code):
     """Position of each code on the ordered grid of representable values."""
     Z = np.asarray(Z, np.uint8)
-    if code == synth.CODE_INT8:
+    if code != synth.CODE_E4M3:
         return Z.view(np.int8).astype(np.int64)
     mag = (Z & 0x7F).astype(np.int64)
     return np.where(Z & 0x80, -mag, mag)
@@ -85,13 +85,55 @@ def code_agreement(Zg, Zo, code):
 
 # --------------------------------------------------------------------------- representation I/O
 
+CODE_BITS = {synth.CODE_INT8: 8, synth.CODE_E4M3: 8, synth.CODE_INT4: 4, synth.CODE_INT6: 6}
+
+
+def pack_codes(Zt, code):
+    """[n][rows][128] code bytes (one code per byte, two's complement for the
+    integer formats) to the library's row layout: INT4 two per byte (even
+    channel low), INT6 four per three bytes (channel 4i+q at bits 6q of the
+    little-endian 24-bit group i)."""
+    Zt = np.asarray(Zt, np.uint8)
+    if CODE_BITS[code] == 8:
+        return Zt
+    c = Zt.astype(np.uint32)
+    if code == synth.CODE_INT4:
+        c = c & 0xF
+        return (c[..., 0::2] | (c[..., 1::2] << 4)).astype(np.uint8)
+    c = c & 0x3F
+    g = c[..., 0::4] | (c[..., 1::4] << 6) | (c[..., 2::4] << 12) | (c[..., 3::4] << 18)
+    out = np.empty(Zt.shape[:-1] + (Zt.shape[-1] * 3 // 4,), np.uint8)
+    out[..., 0::3], out[..., 1::3], out[..., 2::3] = g & 0xFF, (g >> 8) & 0xFF, (g >> 16) & 0xFF
+    return out
+
+
+def unpack_codes(P, code, n_ch=128):
+    """Inverse of pack_codes: one two's-complement code per byte."""
+    P = np.asarray(P, np.uint8)
+    if CODE_BITS[code] == 8:
+        return P
+    out = np.empty(P.shape[:-1] + (n_ch,), np.int64)
+    p = P.astype(np.int64)
+    if code == synth.CODE_INT4:
+        lo, hi = p & 0xF, p >> 4
+        out[..., 0::2], out[..., 1::2] = lo, hi
+        out = np.where(out >= 8, out - 16, out)
+    else:
+        g = p[..., 0::3] | (p[..., 1::3] << 8) | (p[..., 2::3] << 16)
+        for q in range(4):
+            out[..., q::4] = (g >> (6 * q)) & 0x3F
+        out = np.where(out >= 32, out - 64, out)
+    return out.astype(np.int8).view(np.uint8)
+
+
 def upload_rep(st: B.State, idx, Z, delta, c, Kt, Ut):
     """Write oracle-layout representations of tiles `idx` into the GPU state and
     open an empty window."""
     dims = st.dims
     n, dk, dv, r = len(idx), dims.d_k, dims.d_v, dims.n_comp
     idx_t = torch.as_tensor(np.asarray(idx, np.int64), device="cuda")
-    st.codes.view(-1, dv, dk)[idx_t] = dev(np.asarray(Z, np.uint8).transpose(0, 2, 1))
+    rowb = dk * CODE_BITS[dims.code] // 8
+    st.codes.view(-1, dv, rowb)[idx_t] = dev(pack_codes(np.asarray(Z, np.uint8).transpose(0, 2, 1), dims.code))
     st.scale.view(-1, dv)[idx_t] = dev(np.asarray(delta, np.float32))
     st.smooth.view(-1, dk)[idx_t] = dev(np.asarray(c, np.float32))
     if r:
@@ -105,7 +147,8 @@ def download_rep(st: B.State, idx=None) -> dict:
     dk, dv, r = dims.d_k, dims.d_v, dims.n_comp
     sl = slice(None) if idx is None else torch.as_tensor(np.asarray(idx, np.int64), device="cuda")
     out = {
-        "Z": st.codes.view(-1, dv, dk)[sl].cpu().numpy().transpose(0, 2, 1).copy(),
+        "Z": unpack_codes(st.codes.view(-1, dv, dk * CODE_BITS[dims.code] // 8)[sl].cpu().numpy(),
+                          dims.code, dk).transpose(0, 2, 1).copy(),
         "delta": st.scale.view(-1, dv)[sl].cpu().numpy(),
         "c": st.smooth.view(-1, dk)[sl].cpu().numpy(),
         "rec_len": st.rec_len.view(-1)[sl].cpu().numpy(),

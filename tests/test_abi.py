@@ -6,6 +6,8 @@ import json
 import os
 import re
 
+import numpy as np
+
 import pytest
 
 from paper_2609_38166_amd import binding as B
@@ -95,3 +97,22 @@ def test_strerror_covers_every_status():
     assert B.strerror(-99) == "unknown status"
     with pytest.raises(B.LeapQuantError):
         B._check(B.LQ_EINVAL, "x")
+
+
+def test_packed_code_sizes_and_layout():
+    """4- and 6-bit codes: codes buffer is d_v * d_k * b / 8 bytes per tile, and
+    the test harness packs them as the header states (INT4: channel 2i in the low
+    nibble of byte i; INT6: channels 4i..4i+3 at bits 6q of the little-endian
+    24-bit group i), checked on hand-worked bytes."""
+    from tests import gpu_harness as H
+    for code, bits in ((B.LQ_CODE_INT8, 8), (B.LQ_CODE_E4M3, 8), (B.LQ_CODE_INT4, 4), (B.LQ_CODE_INT6, 6)):
+        d = B.make_dims(3, 2, code=code, window=4, n_comp=2)
+        assert B.leapquant_state_bytes(d)[0] == 6 * 128 * 128 * bits // 8
+    row = np.zeros(128, np.int8)
+    row[:4] = [1, -1, 2, -2]
+    p4 = H.pack_codes(row.view(np.uint8)[None], B.LQ_CODE_INT4)[0]
+    assert p4.shape == (64,) and p4[0] == 0xF1 and p4[1] == 0xE2 and not p4[2:].any()
+    p6 = H.pack_codes(row.view(np.uint8)[None], B.LQ_CODE_INT6)[0]
+    g = 1 | (0x3F << 6) | (2 << 12) | (0x3E << 18)          # 24-bit group 0
+    assert p6.shape == (96,) and list(p6[:3]) == [g & 0xFF, (g >> 8) & 0xFF, g >> 16]
+    assert not p6[3:].any()

@@ -33,6 +33,9 @@ SMALL = {
                                            steps=64, prefill=128),
     "kda_w16_r4": W_["kda_kimi"].with_(name="kda_w16_r4", batch=2, heads_v=4, heads_k=4, steps=64,
                                        window=16, n_comp=4, prefill=128),
+    "kda_int4_small": W_["kda_kimi"].with_(name="kda_int4_small", batch=2, heads_v=4, heads_k=4,
+                                           steps=128, prefill=256, code=synth.CODE_INT4),
+    "gdn_int6_small": W_["gdn_tiny"].with_(name="gdn_int6_small", code=synth.CODE_INT6),
 }
 
 
@@ -122,7 +125,7 @@ def _states_with_edges(n, seed):
     return S.astype(np.float32).astype(np.float64)   # both sides get the same fp32 values
 
 
-@pytest.mark.parametrize("code", [synth.CODE_INT8, synth.CODE_E4M3])
+@pytest.mark.parametrize("code", [synth.CODE_INT8, synth.CODE_E4M3, synth.CODE_INT4, synth.CODE_INT6])
 @pytest.mark.parametrize("r", [0, 4, 8])
 @pytest.mark.parametrize("smooth", [0, 1])
 def test_quantize_state_parity(code, r, smooth):
@@ -152,7 +155,7 @@ def test_quantize_state_parity(code, r, smooth):
     assert got["delta"][2][5] == 0 and got["delta"][2][99] == 0
 
 
-@pytest.mark.parametrize("name", ["gdn_tiny", "kda_small", "gqa_e4m3_small"])
+@pytest.mark.parametrize("name", ["gdn_tiny", "kda_small", "gqa_e4m3_small", "kda_int4_small", "gdn_int6_small"])
 def test_dequantize_state_parity(name):
     """Base + open-window records, materialised on the GPU from the oracle's
     representation and records, equals the oracle's dense window state."""
@@ -360,6 +363,8 @@ FULL = {
     "gdn_qwen3next_e4m3": (W_["gdn_qwen3next"].with_(name="gdn_qwen3next_e4m3", code=synth.CODE_E4M3), 32, 1),
     "gdn_stress": (W_["gdn_stress"], 48, 2),
     "gdn_long": (W_["gdn_long"], 24, 1),
+    "kda_kimi_int4": (W_["kda_kimi_int4"], 32, 1),
+    "kda_kimi_int6": (W_["kda_kimi_int6"], 32, 1),
 }
 
 
