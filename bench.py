@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--workload", default="kda_kimi")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
     ap.add_argument("--no-baselines", action="store_true")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the 6- and 4-bit code variants of the headline layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=8192)
     ap.add_argument("--profile", action="store_true",
@@ -54,15 +56,22 @@ def rec_bytes(wl):
     return 2 * (wl.dk + wl.dv) + 2 * wl.g          # FP16 key, correction, decay
 
 
+CODE_BITS = {0: 8, 1: 8, 2: 4, 3: 6}
+
+
+def code_bytes(wl):
+    return wl.dk * wl.dv * CODE_BITS[wl.code] // 8
+
+
 def decode_bytes(wl, i):
     """Algorithmic bytes of one tile's decode at window position i (1-based)."""
     inputs = 4 * (2 * wl.dk) * wl.heads_k / wl.heads_v + 4 * wl.dv + 4 * wl.g + 4
-    return (wl.dk * wl.dv + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+    return (code_bytes(wl) + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
             + (i - 1) * rec_bytes(wl) + rec_bytes(wl) + inputs + 4 * wl.dv + 8)
 
 
 def rep_bytes(wl):
-    return wl.dk * wl.dv + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+    return code_bytes(wl) + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
 
 
 def commit_bytes(wl, p):
@@ -391,6 +400,26 @@ def main():
                        "commit": round(kt["commit_ms"] * 1e3, 2),
                        "quantize": round(kt["quantize_ms"] * 1e3, 2)},
     }
+
+    if not args.no_variants and wl.name == "kda_kimi":
+        # the same layer with the paper's lower-bit residual codes (same inputs)
+        var = {}
+        for vname in ("kda_kimi_int6", "kda_kimi_int4"):
+            vw = synth.WORKLOADS[vname]
+            vd = B_.make_dims(vw.batch, vw.heads_v, vw.heads_k, window=vw.window, n_comp=vw.n_comp,
+                              power_iters=vw.power_iters, gate=vw.gate, code=vw.code)
+            vk = per_launch_times(vw, vd, S0, toks)
+            vstep = (vk["decode_ms"] * vw.steps + vk["commit_ms"] * (vw.steps // vw.window)
+                     + vk["quantize_ms"])
+            vb = float(np.mean([decode_bytes(vw, i) for i in range(1, vw.window + 1)])) * vw.tiles
+            var[vname] = {"value": round(vw.tiles * vw.steps / (vstep * 1e-3), 1),
+                          "ms_per_step_from_kernels": round(vstep, 3),
+                          "decode_us": round(vk["decode_ms"] * 1e3, 2),
+                          "commit_us": round(vk["commit_ms"] * 1e3, 2),
+                          "decode_bytes_per_launch": round(vb),
+                          "decode_gbps": round(vb / (vk["decode_ms"] * 1e-3) / 1e9, 1)}
+            log(f"[bench] {vname}: {var[vname]}")
+        out["code_variants"] = var
 
     if not args.no_baselines:
         q, k, v, a, b = toks

@@ -70,6 +70,16 @@ struct RecRegs {
 
 // Issue the loads of the records in [lo, hi) that belong to slot ts: record
 // hi-1-(PER_SLOT*ts+q) goes to register set q (newest first).
+// y = Gamma_{1:i} x and w = c . y for x = k_t, q_t (thread t < D: channel t).
+__device__ __forceinline__ void write_base_vectors(float G, float kx, float qx, float cs, float (*s_y)[D],
+                                                   float (*s_w)[D], int t) {
+    const float yk = G * kx, yq = G * qx;
+    s_y[0][t] = yk;
+    s_y[1][t] = yq;
+    s_w[0][t] = cs * yk;
+    s_w[1][t] = cs * yq;
+}
+
 // 16 consecutive codes of a row: 16 bytes (byte formats), 8 (INT4) or 12 (INT6).
 template <int CODE>
 __device__ __forceinline__ uint4 load_codes16(const uint8_t *p) {
@@ -243,6 +253,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
                     }
                 }
                 carry = c;
+                if (lo == 0) write_base_vectors(carry, kx, qx, cs, s_y, s_w, tid);   // carry = Gamma_{1:i}
             }
             __syncthreads();
             if (GATE) {
@@ -310,15 +321,11 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         }
     }
 
-    // ---- carry is now Gamma_{1:i}: base and token read vectors -------------------
-    if (tid < D) {
-        const float yk = carry * s_x[0][tid], yq = carry * s_x[1][tid];
-        s_y[0][tid] = yk;
-        s_y[1][tid] = yq;
-        s_w[0][tid] = cs * yk;
-        s_w[1][tid] = cs * yq;
+    // ---- base and token read vectors (written with the last scan when n > 0) -----
+    if (n == 0) {
+        if (tid < D) write_base_vectors(carry, kx, qx, cs, s_y, s_w, tid);
+        __syncthreads();
     }
-    __syncthreads();
 
     // ---- quantized residual: rows rg + 32m, channels 16*g8 .. +15 ---------------
     {
