@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--workload", default="kda_kimi")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
     ap.add_argument("--no-baselines", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="kernel-speed sweep mirroring the paper's ablations (GDN, batch 256): "
+                         "per-step vs per-window codes, Compensator Tokens, smoothing, window and "
+                         "token counts; one JSON line per configuration")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the 6- and 4-bit code variants of the headline layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -328,6 +332,63 @@ def cpu_baseline(wl, n_tiles):
                       f"quantize + decode + commits in fp64, {dt:.2f} s"}
 
 
+# ----------------------------------------------------------------------------- sweep
+
+SWEEP = (  # label, W, r, smooth  (INT8 codes)
+    ("int8 per-step", 1, 0, 0),
+    ("int8 per-window", 16, 0, 0),
+    ("+ compensator tokens", 16, 4, 0),
+    ("+ smoothing (LeapQuant)", 16, 4, 1),
+    ("window 4", 4, 4, 1), ("window 8", 8, 4, 1), ("window 32", 32, 4, 1), ("window 64", 64, 4, 1),
+    ("tokens 2", 16, 2, 1), ("tokens 8", 16, 8, 1), ("tokens 16", 16, 16, 1),
+)
+
+
+def sweep(args):
+    """Per-step cost of each configuration on a GDN layer at batch 256 (32 value
+    heads, 16 key heads, d = 128): average decode launch over one window plus the
+    window's commit divided by W, against the per-step fp32 and bf16 baselines."""
+    import torch
+    from paper_2609_38166_amd import binding as B_, synth
+    base = synth.WORKLOADS["gdn_qwen3next"].with_(name="gdn_b256", batch=256, steps=64)
+    dims0 = B_.make_dims(base.batch, base.heads_v, base.heads_k, window=64, n_comp=4,
+                         power_iters=base.power_iters, gate=base.gate, code=base.code)
+    toks = device_tokens(base, synth.PHASE_DECODE, 64)
+    S0 = prefill_state(base, dims0)
+    q, k, v, a, b = toks
+    res = {}
+    for name, dtype, width, tdt in (("fp32", B_.LQ_STATE_F32, 4, torch.float32),
+                                    ("bf16", B_.LQ_STATE_BF16, 2, torch.bfloat16)):
+        S = S0.to(tdt).contiguous()
+        o = torch.empty((base.batch, base.heads_v, base.dv), dtype=torch.float32, device="cuda")
+
+        def run(S=S, o=o, dtype=dtype):
+            for t in range(64):
+                B_.leapquant_baseline_step(dims0, S, dtype, q[t], k[t], v[t], a[t], b[t], o)
+        run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run()
+        bs, _ = time_steps(g.replay, 3, 1)
+        res[name] = bs / (3 * 64) * 1e6
+        print(json.dumps({"sweep": f"{name} per-step", "us_per_step": round(res[name], 2),
+                          "speedup_vs_fp32": round(res["fp32"] / res[name], 3)}), flush=True)
+        del S
+    for label, W, r, smooth in SWEEP:
+        wl = base.with_(window=W, n_comp=r, smooth=smooth)
+        dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=W, n_comp=r,
+                            power_iters=wl.power_iters, gate=wl.gate, code=wl.code, smooth=smooth)
+        kt = per_launch_times(wl, dims, S0, toks)
+        step = kt["decode_ms"] * 1e3 + kt["commit_ms"] * 1e3 / W
+        print(json.dumps({"sweep": label, "window": W, "n_comp": r, "smooth": smooth,
+                          "decode_us": round(kt["decode_ms"] * 1e3, 2),
+                          "commit_us": round(kt["commit_ms"] * 1e3, 2),
+                          "us_per_step": round(step, 2),
+                          "speedup_vs_fp32": round(res["fp32"] / step, 3),
+                          "speedup_vs_bf16": round(res["bf16"] / step, 3)}), flush=True)
+
+
 # ----------------------------------------------------------------------------- main
 
 def main():
@@ -340,6 +401,9 @@ def main():
     from paper_2609_38166_amd import binding as B_, synth
     B_.lib()
     torch.cuda.set_device(0)
+    if args.sweep:
+        sweep(args)
+        return
     wl = synth.WORKLOADS[args.workload]
     dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=wl.window, n_comp=wl.n_comp,
                         power_iters=wl.power_iters, gate=wl.gate, code=wl.code)

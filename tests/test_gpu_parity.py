@@ -36,6 +36,12 @@ SMALL = {
     "kda_int4_small": W_["kda_kimi"].with_(name="kda_int4_small", batch=2, heads_v=4, heads_k=4,
                                            steps=128, prefill=256, code=synth.CODE_INT4),
     "gdn_int6_small": W_["gdn_tiny"].with_(name="gdn_int6_small", code=synth.CODE_INT6),
+    # corners of the window / token / smoothing sweeps (the paper's ablations)
+    "per_step_w1": W_["gdn_tiny"].with_(name="per_step_w1", steps=24, window=1, n_comp=0, smooth=0),
+    "w4_r2": W_["gdn_tiny"].with_(name="w4_r2", steps=64, window=4, n_comp=2),
+    "w8_r16": W_["gdn_tiny"].with_(name="w8_r16", steps=64, window=8, n_comp=16),
+    "w32_r4_nosmooth": W_["kda_kimi"].with_(name="w32_r4_nosmooth", batch=2, heads_v=4, heads_k=4,
+                                            steps=64, window=32, n_comp=4, smooth=0, prefill=128),
 }
 
 
