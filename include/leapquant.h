@@ -56,6 +56,9 @@ extern "C" {
 #define LQ_CODE_E4M3   1     /* OCP FP8 E4M3FN codes, dequant = e4m3(code) * delta_v  */
 #define LQ_CODE_INT4   2     /* symmetric 4-bit, |code| <= 7, two codes per byte      */
 #define LQ_CODE_INT6   3     /* symmetric 6-bit, |code| <= 31, four codes per 3 bytes  */
+#define LQ_RULE_DELTA  0     /* delta rule: b_t = D_t k_t (DeltaNet, GDN, KDA)        */
+#define LQ_RULE_ADD    1     /* b_t = 0: u_t = v_t (linear attention, RetNet, Mamba2,
+                              * GLA / RWKV6 / HGRN2 with the matching gate)           */
 #define LQ_STATE_F32   0     /* baseline state in fp32                               */
 #define LQ_STATE_BF16  1     /* baseline state in bf16, rounded to nearest even      */
 
@@ -81,6 +84,8 @@ typedef struct {
     int32_t gate;        /* LQ_GATE_SCALAR or LQ_GATE_DIAG                            */
     int32_t code;        /* LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4 or LQ_CODE_INT6  */
     int32_t smooth;      /* 1: residual smoothing (Sec. 3.4); 0: c = 1               */
+    int32_t rule;        /* LQ_RULE_DELTA or LQ_RULE_ADD: the read vector b_t of the
+                          * general recurrence (App. A instance table)               */
 } lq_dims;
 
 /* The quantized state of all tiles (device pointers, caller-owned).

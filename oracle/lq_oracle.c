@@ -17,7 +17,8 @@
  *
  *   O1  recurrence, Sec. 3.1 Eq. (general) with the GDN / KDA rows of the
  *       instance table (App. A): A = D_t S, u = v - A^T k, S = A + beta k u^T,
- *       o = S^T q.  Because the read vector is b = alpha k (GDN) or alpha.k
+ *       o = S^T q.  The rows with b_t = 0 (linear attention, RetNet, Mamba2,
+ *       GLA / RWKV6 / HGRN2) drop the read: u = v (cfg->rule = 1).  Because the read vector is b = alpha k (GDN) or alpha.k
  *       (KDA) and D_t is diagonal, S_{t-1}^T b = (D_t S_{t-1})^T k.
  *   O2  quantizer: Compensator Tokens (Sec. 3.3, Eqs. (compensator),
  *       (compensator-rank-r)), fitted by power iteration (Sec. 4.1), then
@@ -68,6 +69,7 @@ typedef struct {
     int32_t smooth;        /* 1: residual smoothing; 0: c = 1 */
     int32_t quantize;      /* 1: quantize at window ends; 0: keep the state exact */
     int32_t round_records; /* 1: FP16 records (alpha, write key, correction); 0: exact */
+    int32_t rule;          /* 0: delta rule (b_t = D_t k_t); 1: additive (b_t = 0) */
 } lqo_cfg;
 
 enum { LQO_STATE_EXACT = 0, LQO_STATE_F32 = 1, LQO_STATE_BF16 = 2 };
@@ -269,7 +271,8 @@ static void recurrent_step_impl(const lqo_cfg *cfg, real *S, const float *q, con
     }
     for (int v = 0; v < dv; ++v) {
         real s = 0;
-        for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];     /* A^T k */
+        if (cfg->rule == 0)
+            for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];  /* A^T k */
         w[v] = (real)vv[v] - s;                                             /* u */
     }
     for (int i = 0; i < dk; ++i) {
@@ -315,7 +318,8 @@ static void window_step_impl(const lqo_cfg *cfg, real *S, const float *q, const 
     }
     for (int v = 0; v < dv; ++v) {
         real s = 0;
-        for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];
+        if (cfg->rule == 0)
+            for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];
         u[v] = rec_round(cfg, (real)vv[v] - s);                             /* u_i = v_i - A_i^T k_i */
         ru[v] = (double)u[v];
     }
@@ -424,7 +428,7 @@ void OQ(readout_step)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, 
         kq += tk * (real)q[i];
     }
     for (int v = 0; v < dv; ++v) {
-        real u = rec_round(cfg, (real)vv[v] - Ak[v]);
+        real u = rec_round(cfg, (real)vv[v] - (cfg->rule == 0 ? Ak[v] : (real)0));
         nu[v] = (double)u;
         o[v] = (double)(Aq[v] + u * kq);                                     /* S_i^T q */
     }

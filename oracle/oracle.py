@@ -36,7 +36,7 @@ def lib():
 class Cfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "dk", "dv", "window", "n_comp", "power_iters", "gate", "code", "smooth",
-        "quantize", "round_records")]
+        "quantize", "round_records", "rule")]
 
 
 class _Inputs(C.Structure):
@@ -50,13 +50,14 @@ class _Outputs(C.Structure):
 
 
 GATE_SCALAR, GATE_DIAG = 0, 1
+RULE_DELTA, RULE_ADD = 0, 1    # b_t = D_t k_t (delta rule) or b_t = 0
 CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6 = 0, 1, 2, 3
 STATE_EXACT, STATE_F32, STATE_BF16 = 0, 1, 2
 
 
 def make_cfg(dk=128, dv=128, window=16, n_comp=4, power_iters=4, gate=GATE_SCALAR,
-             code=CODE_INT8, smooth=1, quantize=1, round_records=1) -> Cfg:
-    return Cfg(dk, dv, window, n_comp, power_iters, gate, code, smooth, quantize, round_records)
+             code=CODE_INT8, smooth=1, quantize=1, round_records=1, rule=RULE_DELTA) -> Cfg:
+    return Cfg(dk, dv, window, n_comp, power_iters, gate, code, smooth, quantize, round_records, rule)
 
 
 def _p(a):

@@ -20,6 +20,7 @@ LQ_GATE_SCALAR, LQ_GATE_DIAG = 0, 1
 LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4, LQ_CODE_INT6 = 0, 1, 2, 3
 CODE_BITS = {LQ_CODE_INT8: 8, LQ_CODE_E4M3: 8, LQ_CODE_INT4: 4, LQ_CODE_INT6: 6}
 LQ_STATE_F32, LQ_STATE_BF16 = 0, 1
+LQ_RULE_DELTA, LQ_RULE_ADD = 0, 1
 LQ_DEVERR_WINDOW_FULL = 1
 LQ_DEVERR_BAD_REC_LEN = 2
 
@@ -40,7 +41,7 @@ class LeapQuantError(RuntimeError):
 class lq_dims(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "batch", "heads_v", "heads_k", "d_k", "d_v", "window", "n_comp", "power_iters", "gate",
-        "code", "smooth")]
+        "code", "smooth", "rule")]
 
 
 class lq_state(C.Structure):
@@ -140,9 +141,10 @@ def _stream(stream):
 
 
 def make_dims(batch, heads_v, heads_k=None, window=16, n_comp=4, power_iters=4,
-              gate=LQ_GATE_SCALAR, code=LQ_CODE_INT8, smooth=1, d_k=128, d_v=128) -> lq_dims:
+              gate=LQ_GATE_SCALAR, code=LQ_CODE_INT8, smooth=1, d_k=128, d_v=128,
+              rule=LQ_RULE_DELTA) -> lq_dims:
     return lq_dims(batch, heads_v, heads_k or heads_v, d_k, d_v, window, n_comp, power_iters, gate,
-                   code, smooth)
+                   code, smooth, rule)
 
 
 FIELDS = ("codes", "scale", "smooth", "comp_k", "comp_u", "rec_k", "rec_u", "rec_a", "rec_len", "err")

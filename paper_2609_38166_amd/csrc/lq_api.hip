@@ -38,6 +38,7 @@ int32_t check_dims(const lq_dims *d) {
         d->code != LQ_CODE_INT6)
         return LQ_EINVAL;
     if (d->smooth != 0 && d->smooth != 1) return LQ_EINVAL;
+    if (d->rule != LQ_RULE_DELTA && d->rule != LQ_RULE_ADD) return LQ_EINVAL;
     if (d->d_k != 128 || d->d_v != 128) return LQ_EUNSUPPORTED;
     if (d->n_comp > LQ_MAX_COMP) return LQ_EUNSUPPORTED;
     if (d->n_comp > 0 && (d->power_iters < 1 || d->power_iters > LQ_MAX_POWER_ITERS))

@@ -1,5 +1,6 @@
 // Per-step baseline with a dense fp32 or bf16 state (Sec. 4.1 "Baselines"):
 //   A = D S,  u = v - A^T k,  S = A + (beta k) u^T,  o = S^T q   (Sec. 3.1)
+// (u = v for the b_t = 0 rows of the instance table, App. A)
 // One 256-thread workgroup per tile; 16 lanes cover one 128-entry state row
 // S^T[v][:] (8 key channels each), so both matvecs are DPP row reductions.
 // The state is read once and written once; arithmetic is fp32, a bf16 state is
@@ -24,7 +25,7 @@ struct BaseArgs {
     int group;
 };
 
-template <int GATE, int BF16>
+template <int GATE, int BF16, int RULE>
 __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -91,7 +92,8 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
             s[m][j] *= al[j];                           // A = D S
             p = fmaf(s[m][j], kx[j], p);
         }
-        const float u = a.v[tvec + vrow] - row16_sum(p);  // u = v - A^T k
+        const float u = RULE == LQ_RULE_ADD ? a.v[tvec + vrow]
+                                            : a.v[tvec + vrow] - row16_sum(p);  // u = v - A^T k
         float po = 0.0f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -127,8 +129,11 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
 }
 
 template <int GATE, int BF16>
-hipError_t launch(const BaseArgs &a, int tiles, hipStream_t st) {
-    hipLaunchKernelGGL((baseline_kernel<GATE, BF16>), dim3(tiles), dim3(NT), 0, st, a);
+hipError_t launch(const BaseArgs &a, int tiles, int rule, hipStream_t st) {
+    if (rule == LQ_RULE_ADD)
+        hipLaunchKernelGGL((baseline_kernel<GATE, BF16, LQ_RULE_ADD>), dim3(tiles), dim3(NT), 0, st, a);
+    else
+        hipLaunchKernelGGL((baseline_kernel<GATE, BF16, LQ_RULE_DELTA>), dim3(tiles), dim3(NT), 0, st, a);
     return hipGetLastError();
 }
 
@@ -148,8 +153,9 @@ hipError_t launch_baseline(const lq_dims &d, void *S, int state_dtype, const Tok
     a.group = d.heads_v / d.heads_k;
     const int tiles = d.batch * d.heads_v;
     const bool bf = state_dtype == LQ_STATE_BF16;
-    if (d.gate == LQ_GATE_DIAG) return bf ? launch<1, 1>(a, tiles, st) : launch<1, 0>(a, tiles, st);
-    return bf ? launch<0, 1>(a, tiles, st) : launch<0, 0>(a, tiles, st);
+    if (d.gate == LQ_GATE_DIAG)
+        return bf ? launch<1, 1>(a, tiles, d.rule, st) : launch<1, 0>(a, tiles, d.rule, st);
+    return bf ? launch<0, 1>(a, tiles, d.rule, st) : launch<0, 0>(a, tiles, d.rule, st);
 }
 
 }  // namespace lq

@@ -108,7 +108,7 @@ __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, 
     }
 }
 
-template <int GATE, int CODE>
+template <int GATE, int CODE, int RULE>
 __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     constexpr int G = GATE ? D : 1;     // decay values per record
     __shared__ float s_x[2][D];          // x = k_t, q_t
@@ -390,7 +390,9 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             ak += u_.red[s][0][tid];
             aq += u_.red[s][1][tid];
         }
-        const uint16_t uh = f2h(vx - ak);                  // u_t = fp16(v_t - A^T k_t)
+        // u_t = fp16(v_t - A^T k_t); the b_t = 0 rule reads nothing (the k-side
+        // readouts above are then dead code and compiled out)
+        const uint16_t uh = f2h(RULE == LQ_RULE_ADD ? vx : vx - ak);
         a.rec_u[(rbase + n) * D + tid] = uh;
         a.o[tvec + tid] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
         if (tid == 0) a.rec_len[tile] = n + 1;
@@ -398,8 +400,11 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
 }
 
 template <int GATE, int CODE>
-hipError_t launch(const DecodeArgs &args, hipStream_t st) {
-    hipLaunchKernelGGL((decode_kernel<GATE, CODE>), dim3(args.tiles), dim3(NT), 0, st, args);
+hipError_t launch(const DecodeArgs &args, int rule, hipStream_t st) {
+    if (rule == LQ_RULE_ADD)
+        hipLaunchKernelGGL((decode_kernel<GATE, CODE, LQ_RULE_ADD>), dim3(args.tiles), dim3(NT), 0, st, args);
+    else
+        hipLaunchKernelGGL((decode_kernel<GATE, CODE, LQ_RULE_DELTA>), dim3(args.tiles), dim3(NT), 0, st, args);
     return hipGetLastError();
 }
 
@@ -430,17 +435,17 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
     a.tiles = d.batch * d.heads_v;
     if (d.gate == LQ_GATE_DIAG) {
         switch (d.code) {
-            case LQ_CODE_E4M3: return launch<1, 1>(a, st);
-            case LQ_CODE_INT4: return launch<1, 2>(a, st);
-            case LQ_CODE_INT6: return launch<1, 3>(a, st);
-            default: return launch<1, 0>(a, st);
+            case LQ_CODE_E4M3: return launch<1, 1>(a, d.rule, st);
+            case LQ_CODE_INT4: return launch<1, 2>(a, d.rule, st);
+            case LQ_CODE_INT6: return launch<1, 3>(a, d.rule, st);
+            default: return launch<1, 0>(a, d.rule, st);
         }
     }
     switch (d.code) {
-        case LQ_CODE_E4M3: return launch<0, 1>(a, st);
-        case LQ_CODE_INT4: return launch<0, 2>(a, st);
-        case LQ_CODE_INT6: return launch<0, 3>(a, st);
-        default: return launch<0, 0>(a, st);
+        case LQ_CODE_E4M3: return launch<0, 1>(a, d.rule, st);
+        case LQ_CODE_INT4: return launch<0, 2>(a, d.rule, st);
+        case LQ_CODE_INT6: return launch<0, 3>(a, d.rule, st);
+        default: return launch<0, 0>(a, d.rule, st);
     }
 }
 

@@ -53,14 +53,15 @@ def f16_vals(bits):
 
 def ocfg(wl: synth.Workload, **kw) -> O.Cfg:
     args = dict(dk=wl.dk, dv=wl.dv, window=wl.window, n_comp=wl.n_comp,
-                power_iters=wl.power_iters, gate=wl.gate, code=wl.code, smooth=wl.smooth)
+                power_iters=wl.power_iters, gate=wl.gate, code=wl.code, smooth=wl.smooth,
+                rule=wl.rule)
     args.update(kw)
     return O.make_cfg(**args)
 
 
 def gdims(wl: synth.Workload, **kw) -> B.lq_dims:
     args = dict(window=wl.window, n_comp=wl.n_comp, power_iters=wl.power_iters, gate=wl.gate,
-                code=wl.code, smooth=wl.smooth, d_k=wl.dk, d_v=wl.dv)
+                code=wl.code, smooth=wl.smooth, d_k=wl.dk, d_v=wl.dv, rule=wl.rule)
     args.update(kw)
     return B.make_dims(wl.batch, wl.heads_v, wl.heads_k, **args)
 

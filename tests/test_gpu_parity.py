@@ -42,6 +42,10 @@ SMALL = {
     "w8_r16": W_["gdn_tiny"].with_(name="w8_r16", steps=64, window=8, n_comp=16),
     "w32_r4_nosmooth": W_["kda_kimi"].with_(name="w32_r4_nosmooth", batch=2, heads_v=4, heads_k=4,
                                             steps=64, window=32, n_comp=4, smooth=0, prefill=128),
+    # b_t = 0 rows of the instance table: Mamba2 (scalar decay), GLA / RWKV6 (per-channel)
+    "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1),
+    "gla_small": W_["kda_kimi"].with_(name="gla_small", batch=2, heads_v=4, heads_k=4, steps=128,
+                                      prefill=256, rule=1),
 }
 
 
@@ -61,11 +65,12 @@ def _tokens_random(wl, T, seed):
     return st, tok
 
 
+@pytest.mark.parametrize("rule", [0, 1])
 @pytest.mark.parametrize("gate", [synth.GATE_SCALAR, synth.GATE_DIAG])
 @pytest.mark.parametrize("dtype", [B.LQ_STATE_F32, B.LQ_STATE_BF16])
-def test_baseline_step_parity(gate, dtype):
-    wl = W_["gdn_tiny"].with_(batch=2, heads_v=4, heads_k=2, gate=gate)
-    H.log(f"baseline gate={gate} dtype={dtype}")
+def test_baseline_step_parity(gate, dtype, rule):
+    wl = W_["gdn_tiny"].with_(batch=2, heads_v=4, heads_k=2, gate=gate, rule=rule)
+    H.log(f"baseline gate={gate} dtype={dtype} rule={rule}")
     rng = np.random.default_rng(5)
     S0 = rng.standard_normal((wl.tiles, wl.dk, wl.dv)).astype(np.float32).astype(np.float64)
     if dtype == B.LQ_STATE_BF16:

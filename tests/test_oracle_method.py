@@ -50,6 +50,37 @@ def test_recurrence_equals_native_gdn_kda(O, gate):
         S = native
 
 
+@pytest.mark.parametrize("gate", [0, 1])
+def test_additive_instances_native_forms(O, gate):
+    """Rows of the instance table with b_t = 0 (App. A): S_t = D_t S + k~ v^T with no
+    read of the previous state -- Mamba2 (scalar decay), GLA / RWKV6 / HGRN2
+    (per-channel decay); with D = I and beta = 1 the state of linear attention is
+    the plain sum of k v^T."""
+    rng = np.random.default_rng(14 + gate)
+    dk, dv = 16, 12
+    cfg = O.make_cfg(dk=dk, dv=dv, gate=gate, rule=O.RULE_ADD)
+    S = rng.standard_normal((dk, dv))
+    for _ in range(5):
+        q, k, v = unit(rng, dk), unit(rng, dk), f32(rng.standard_normal(dv))
+        beta = np.float32(rng.uniform(0.1, 0.9))
+        a = f32(rng.uniform(0.5, 1.0, dk if gate else 1))
+        D = np.diag(a.astype(np.float64)) if gate else a[0] * np.eye(dk)
+        native = D @ S + np.float64(beta) * np.outer(k.astype(np.float64), v.astype(np.float64))
+        S_new, o = O.recurrent_step(cfg, S, q, k, v, a, beta)
+        assert rel(S_new, native) < 1e-13
+        assert rel(o, native.T @ q.astype(np.float64)) < 1e-13
+        S = native
+    # linear attention: D = I, beta = 1 -> S_T = S_0 + sum_t k_t v_t^T
+    cl = O.make_cfg(dk=dk, dv=dv, gate=0, rule=O.RULE_ADD)
+    S0 = rng.standard_normal((dk, dv))
+    S, acc = S0.copy(), S0.copy()
+    for _ in range(6):
+        q, k, v = unit(rng, dk), unit(rng, dk), f32(rng.standard_normal(dv))
+        S, _ = O.recurrent_step(cl, S, q, k, v, f32([1.0]), 1.0)
+        acc += np.outer(k.astype(np.float64), v.astype(np.float64))
+    assert rel(S, acc) < 1e-14
+
+
 def test_delta_rule_writes_value_exactly(O):
     """alpha = 1, beta = 1, |k| = 1: after the write S^T k = v (the delta rule)."""
     rng = np.random.default_rng(11)
@@ -281,14 +312,17 @@ def _tokens(rng, tiles, T, dk, dv, gate):
 
 @pytest.mark.parametrize("gate", [0, 1])
 @pytest.mark.parametrize("W", [1, 3, 16])
-def test_window_unrolling_equals_recurrence(O, gate, W):
+@pytest.mark.parametrize("rule", [0, 1])
+def test_window_unrolling_equals_recurrence(O, gate, W, rule):
     """Quantization off and exact records: the per-window method (both forms) is
-    the recurrence itself (Eq. (window) follows from Eq. (record) by induction)."""
-    rng = np.random.default_rng(50 + W + gate)
+    the recurrence itself (Eq. (window) follows from Eq. (record) by induction),
+    for the delta rule and for the b_t = 0 rows of the instance table."""
+    rng = np.random.default_rng(50 + W + gate + 7 * rule)
     dk = dv = 32
     S0 = rng.standard_normal((3, dk, dv))
     tok = _tokens(rng, 3, 37, dk, dv, gate)
-    cfg = O.make_cfg(dk=dk, dv=dv, window=W, n_comp=2, gate=gate, quantize=0, round_records=0)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=W, n_comp=2, gate=gate, quantize=0, round_records=0,
+                     rule=rule)
     o_ref, S_ref = O.run_baseline(cfg, S0, tok, mode=O.STATE_EXACT)
     for run in (O.run_dense, O.run_readout):
         res = run(cfg, S0, tok, snapshots=False)
@@ -324,12 +358,14 @@ def test_window_one_without_tokens_is_naive_per_step(O, smooth):
                                                 (1, 0, 0, 0), (0, 0, 2, 0)])
 def test_readout_form_equals_dense_form(O, gate, code, r, smooth):
     """Buffered readout (App. B.2-B.3) from the fixed quantized base equals the
-    dense step-by-step window, at every token and every window end."""
+    dense step-by-step window, at every token and every window end (the delta
+    rule, and the b_t = 0 rule on the odd cases)."""
     rng = np.random.default_rng(70 + gate + 2 * code + r)
     dk = dv = 64
     S0 = _state(rng, dk, dv)[None].repeat(2, 0) * rng.uniform(0.5, 2, (2, 1, 1))
     tok = _tokens(rng, 2, 45, dk, dv, gate)
-    cfg = O.make_cfg(dk=dk, dv=dv, window=16, n_comp=r, gate=gate, code=code, smooth=smooth)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=16, n_comp=r, gate=gate, code=code, smooth=smooth,
+                     rule=(r + code + gate) % 2)
     d, b = O.run_dense(cfg, S0, tok), O.run_readout(cfg, S0, tok)
     assert rel(b["o"], d["o"]) < 1e-10
     assert np.mean(b["Z"] == d["Z"]) > 0.9999
