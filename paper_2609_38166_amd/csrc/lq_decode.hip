@@ -10,11 +10,11 @@
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
 //
 // Every global load of the tile is issued before the first barrier, those that
-// do not depend on rec_len first: the token inputs, the d_v x d_k codes (16
-// codes per lane: 16, 12 or 8 bytes for 8-, 6- or 4-bit codes, 8 lanes per
-// row), the compensators, then rec_len and
-// one pass of records (16 slots of 16 lanes, each slot a contiguous block of
-// records, 16 bytes of key, correction and decay per lane).  The decays
+// do not depend on rec_len first: the token inputs, the d_v x d_k codes (copied
+// straight into LDS, 16 bytes per lane and instruction, so they hold no
+// registers), the compensators, then rec_len and one pass of records (16 slots
+// of 16 lanes, each slot a contiguous block of records, 16 bytes of key,
+// correction and decay per lane).  The decays
 // Gamma_{j+1:i} are products of the FP16 record decays: each slot forms the
 // product of its block, one scan over the 16 slots gives every block the decay
 // of all newer records, and the slot walks its block from the newest record
@@ -28,12 +28,28 @@ namespace {
 
 constexpr int SLOTS = 16;            // 16-lane groups per workgroup
 // Records per slot and pass: the diagonal gate carries a 16-byte decay per lane
-// and record, so it holds two per slot (32 per pass) to stay at 4 resident
-// workgroups per CU; the scalar gate holds four (64 per pass).
+// and record, so it holds PS_DIAG per slot to stay within 128 VGPRs (4 resident
+// workgroups per CU); the scalar gate holds four (64 per pass).
+#ifndef LQ_PS_DIAG
+#define LQ_PS_DIAG 3
+#endif
 template <int GATE> struct Pass {
-    static constexpr int PER_SLOT = GATE ? 2 : 4;
+    static constexpr int PER_SLOT = GATE ? LQ_PS_DIAG : 4;
     static constexpr int N = SLOTS * PER_SLOT;
 };
+
+// Per-channel vectors that the slots read or write 8 channels at a time are
+// kept in LDS in a swizzled order: channel 8*l16 + j sits at position
+// 16*j + l16, so for each j the 16 lanes of a slot touch 16 consecutive words.
+// Per-slot rows are padded by 16 words, which puts the 4 slots of a wave in
+// different bank groups.  A thread t < D that works on a whole vector (the
+// scan, the base vectors, the final combine) owns position t, i.e. channel
+// CH(t); POS is the inverse map.
+constexpr int RP = D + 16;                       // padded per-slot row
+__device__ __forceinline__ constexpr int SW(int l16, int j) { return 16 * j + l16; }
+__device__ __forceinline__ constexpr int CH(int t) { return 8 * (t & 15) + (t >> 4); }
+__device__ __forceinline__ constexpr int POS(int c) { return 16 * (c & 7) + (c >> 3); }
+static_assert(CH(POS(77)) == 77 && POS(CH(77)) == 77, "CH and POS are inverse");
 
 struct DecodeArgs {
     const uint8_t *codes;
@@ -65,19 +81,52 @@ struct RecRegs {
     uint4 k[PER_SLOT];               // FP16 keys, 8 channels
     uint4 u[PER_SLOT];               // FP16 corrections, 8 values
     uint4 a[GATE ? PER_SLOT : 1];    // FP16 decays, 8 channels (diagonal gate)
-    float as[PER_SLOT];              // decay (scalar gate)
+    uint32_t as[PER_SLOT];           // FP16 decay (scalar gate), converted where used
 };
 
-// Issue the loads of the records in [lo, hi) that belong to slot ts: record
-// hi-1-(PER_SLOT*ts+q) goes to register set q (newest first).
-// y = Gamma_{1:i} x and w = c . y for x = k_t, q_t (thread t < D: channel t).
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// Copy 16 bytes per lane from global memory straight into LDS: lane L of the
+// wave writes lds_base + 16 L (lds_base uniform).  Issued from asm so that the
+// compiler does not treat it as an LDS store that every later LDS access must
+// wait for; the reader waits with wait_vm_all() and a barrier.  This kernel
+// uses M0 for nothing else.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(g), "s"(lds_base) : "memory");
+}
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Sum of x over the 4 slots (16-lane rows) of a wave, for 8 values per lane,
+// as a reduce-scatter: lane (row rho, l16) returns the sums of values 2 rho
+// and 2 rho + 1.  A cross-row swap of registers (a, b) hands the lower rows
+// the upper rows' a and the upper rows the lower rows' b, so own + received is
+// the sum wanted in every lane without a select.
+__device__ __forceinline__ void rows4_reduce_scatter(const float *x, float &s0, float &s1) {
+    float h[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {           // rows rho, rho ^ 2: keep values 4 (rho >> 1) + 0..3
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[i]), __float_as_uint(x[4 + i]), false, false);
+        h[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    // rows rho, rho ^ 1: keep 2 of those 4
+    const auto r0 = __builtin_amdgcn_permlane16_swap(__float_as_uint(h[0]), __float_as_uint(h[2]), false, false);
+    const auto r1 = __builtin_amdgcn_permlane16_swap(__float_as_uint(h[1]), __float_as_uint(h[3]), false, false);
+    s0 = __uint_as_float(r0[0]) + __uint_as_float(r0[1]);
+    s1 = __uint_as_float(r1[0]) + __uint_as_float(r1[1]);
+}
+
+// y = Gamma_{1:i} x (swizzled) and w = c . y (channel order) for x = k_t, q_t;
+// thread t < D: channel CH(t).
 __device__ __forceinline__ void write_base_vectors(float G, float kx, float qx, float cs, float (*s_y)[D],
                                                    float (*s_w)[D], int t) {
     const float yk = G * kx, yq = G * qx;
     s_y[0][t] = yk;
     s_y[1][t] = yq;
-    s_w[0][t] = cs * yk;
-    s_w[1][t] = cs * yq;
+    s_w[0][CH(t)] = cs * yk;
+    s_w[1][CH(t)] = cs * yq;
 }
 
 // 16 consecutive codes of a row: 16 bytes (byte formats), 8 (INT4) or 12 (INT6).
@@ -92,6 +141,8 @@ __device__ __forceinline__ uint4 load_codes16(const uint8_t *p) {
     return make_uint4(w[0], w[1], w[2], 0u);
 }
 
+// Issue the loads of the records in [lo, hi) that belong to slot ts: record
+// hi-1-(PER_SLOT*ts+q) goes to register set q (newest first).
 template <int GATE>
 __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi,
                                              int ts, int l16, RecRegs<GATE> &R) {
@@ -103,26 +154,31 @@ __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, 
             R.k[q] = *(const uint4 *)(a.rec_k + (rbase + r) * D + 8 * l16);
             R.u[q] = *(const uint4 *)(a.rec_u + (rbase + r) * D + 8 * l16);
             if (GATE) R.a[q] = *(const uint4 *)(a.rec_a + (rbase + r) * D + 8 * l16);
-            else R.as[q] = h2f(a.rec_a[rbase + r]);
+            else R.as[q] = a.rec_a[rbase + r];
         }
     }
 }
 
 template <int GATE, int CODE, int RULE>
-__global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
-    constexpr int G = GATE ? D : 1;     // decay values per record
-    __shared__ float s_x[2][D];          // x = k_t, q_t
-    __shared__ float s_w[2][D];          // c . Gamma_{1:i} . x
-    __shared__ float s_y[2][D];          // Gamma_{1:i} . x
-    __shared__ float s_z[2][D];          // quantized-residual readout
+__global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
+    constexpr int GP = GATE ? RP : 1;
+    constexpr int ROWB = D * CodeFmt<CODE>::BITS / 8;   // code bytes per value row
+    constexpr int ZCH = D * ROWB / 16;                   // 16-byte chunks of a tile's codes
+    static_assert(ZCH % NT == 0, "whole chunks per thread");
+    __shared__ float s_x[2][D];          // x = k_t, q_t (swizzled)
+    __shared__ float s_w[2][D];          // c . Gamma_{1:i} . x (channel order)
+    __shared__ float s_y[2][D];          // Gamma_{1:i} . x (swizzled)
+    __shared__ float s_z[2][D];          // quantized-residual readout (swizzled)
     __shared__ float s_kq[2];            // k~_t . q_t (per wave pair)
-    __shared__ union {
-        struct {
-            float bp[SLOTS][G];          // decay product of each slot's block
-            float pre[SLOTS][G];         // decay of everything newer than the block
-        } scan;
-        float red[SLOTS][2][D];          // per-slot partial readouts
-    } u_;
+    // decay product of each slot's block, replaced in place by the decay of
+    // everything newer than the block (swizzled; the diagonal gate's thread t
+    // alone reads and writes position t).  The scalar gate's single product is
+    // read by every scan thread, so its prefix goes to s_pre0 instead.
+    __shared__ float s_bp[SLOTS][GP];
+    __shared__ float s_pre0[SLOTS];
+    __shared__ __align__(16) uint4 s_codes[ZCH];   // the tile's codes, row-major as in HBM
+    __shared__ __align__(16) float s_dlt[D];       // the tile's per-row scales
+    __shared__ __align__(16) float s_red[NT / 64][2][2 * 64];   // per-wave partial readouts, k then q
 
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -136,45 +192,53 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     const int rg = tid >> 3;             // code rows rg, rg+32, rg+64, rg+96
     const size_t rbase = (size_t)tile * a.window;
 
-    // ---- issue every load of the tile: first what does not depend on rec_len ----
-    float kx = 0.0f, qx = 0.0f, cs = 0.0f, al = 0.0f, vx = 0.0f, bt = 0.0f;
+    // ---- issue every load of the tile: rec_len (a scalar load, which the record
+    // loads wait for), then what does not depend on it ---------------------------
+    // (thread t < D: channel ch = CH(t))
+    const int n = a.rec_len[tile];
+    const int ch = CH(tid & (D - 1));
+    // (beta, and alpha of the scalar gate, are per-tile scalars)
+    float bt = a.beta[tile];
+    float al = GATE ? 0.0f : a.alpha[tile];
+    float kx = 0.0f, qx = 0.0f, cs = 0.0f, vx = 0.0f;
     if (tid < D) {
-        kx = a.k[kvec + tid];
-        qx = a.q[kvec + tid];
-        cs = a.smooth[tvec + tid];
-        al = GATE ? a.alpha[tvec + tid] : a.alpha[tile];
-        vx = a.v[tvec + tid];
-        bt = a.beta[tile];
+        kx = a.k[kvec + ch];
+        qx = a.q[kvec + ch];
+        cs = a.smooth[tvec + ch];
+        if (GATE) al = a.alpha[tvec + ch];
+        vx = a.v[tvec + ch];
     }
-    constexpr int ROWB = D * CodeFmt<CODE>::BITS / 8;   // code bytes per value row
-    const uint8_t *zt = a.codes + (size_t)tile * D * ROWB;
-    uint4 zr[4];
+    {
+        // chunk c = NT m + 64 w + L goes to s_codes[c]: wave w's lanes fill 1 KiB
+        const uint4 *zt = (const uint4 *)(a.codes + (size_t)tile * D * ROWB);
+        const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) zr[m] = load_codes16<CODE>(zt + (size_t)(rg + 32 * m) * ROWB + 2 * CodeFmt<CODE>::BITS * g8);
-    float dlt[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (g8 == 0) {
-#pragma unroll
-        for (int m = 0; m < 4; ++m) dlt[m] = a.scale[tvec + rg + 32 * m];
+        for (int m = 0; m < ZCH / NT; ++m) dma16(zt + NT * m + tid, lds_addr(&s_codes[NT * m + 64 * w]));
     }
+    if (tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(s_dlt));   // per-row scales, wave 0
     uint4 ck = make_uint4(0, 0, 0, 0), cu = make_uint4(0, 0, 0, 0);
     if (ts < a.n_comp) {
         const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
         ck = *(const uint4 *)(a.comp_k + cb);
         cu = *(const uint4 *)(a.comp_u + cb);
     }
-    const int n = a.rec_len[tile];
     if (n >= a.window || n < 0) {        // window buffer full (or corrupt): tile untouched
         if (tid == 0) atomicOr(a.err, n < 0 ? (int)LQ_DEVERR_BAD_REC_LEN : (int)LQ_DEVERR_WINDOW_FULL);
         if (tid < D) a.o[tvec + tid] = __builtin_nanf("");
+        wait_vm_all();                   // no copy into LDS outlives the workgroup
         return;
     }
     RecRegs<GATE> R;
     constexpr int PER_SLOT = Pass<GATE>::PER_SLOT, PASS = Pass<GATE>::N;
     int hi = n, lo = n > PASS ? n - PASS : 0;
     load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
+    // Nothing that consumes the token inputs may be scheduled above this point:
+    // a wait for one of them ahead of the code and record loads would delay
+    // every load of the tile by a memory round trip.
+    asm volatile("" : "+v"(kx), "+v"(qx), "+v"(cs), "+v"(al), "+v"(vx), "+v"(bt));
 
     // ---- token inputs, this token's record -------------------------------------
-    // carry: decay of every record newer than the current pass, channel tid
+    // carry: decay of every record newer than the current pass, channel ch
     // (the scalar gate keeps the same product in every thread below D)
     float carry = 1.0f;
     if (tid < D) {
@@ -183,10 +247,10 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         const uint16_t ah = f2h(al);
         carry = h2f(ah);
         const size_t slot = rbase + n;
-        if (GATE) a.rec_a[slot * D + tid] = ah;
+        if (GATE) a.rec_a[slot * D + ch] = ah;
         else if (tid == 0) a.rec_a[slot] = ah;
         const uint16_t tkh = f2h(bt * kx);                   // k~_t = fp16(beta_t k_t)
-        a.rec_k[slot * D + tid] = tkh;
+        a.rec_k[slot * D + ch] = tkh;
         const float kq = wave_sum(h2f(tkh) * qx);
         if ((tid & 63) == 0) s_kq[tid >> 6] = kq;
     }
@@ -213,53 +277,47 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
 #pragma unroll
                         for (int j = 0; j < 8; ++j) bp[j] *= av[j];
                     } else {
-                        bp[0] *= R.as[q];
+                        bp[0] *= h2f((uint16_t)R.as[q]);
                     }
                 }
             }
             if (GATE) {
 #pragma unroll
-                for (int j = 0; j < 8; ++j) u_.scan.bp[ts][8 * l16 + j] = bp[j];
+                for (int j = 0; j < 8; ++j) s_bp[ts][SW(l16, j)] = bp[j];
             } else if (l16 == 0) {
-                u_.scan.bp[ts][0] = bp[0];
+                s_bp[ts][0] = bp[0];
             }
             __syncthreads();
             if (first) {
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    xk[j] = s_x[0][8 * l16 + j];
-                    xq[j] = s_x[1][8 * l16 + j];
+                    xk[j] = s_x[0][SW(l16, j)];
+                    xq[j] = s_x[1][SW(l16, j)];
                 }
                 first = false;
             }
             // exclusive scan over the slots; slot 0 holds the newest block
             if (tid < D) {
-                const int ch = GATE ? tid : 0;
                 float c = carry;
-                if (GATE) {                  // slot products read ahead of the chain
-                    float bv[SLOTS];
+                // slot products read ahead of the chain, then overwritten
+                float bv[SLOTS];
 #pragma unroll
-                    for (int s = 0; s < SLOTS; ++s) bv[s] = u_.scan.bp[s][ch];
+                for (int s = 0; s < SLOTS; ++s) bv[s] = s_bp[s][GATE ? tid : 0];
 #pragma unroll
-                    for (int s = 0; s < SLOTS; ++s) {
-                        u_.scan.pre[s][ch] = c;
-                        c *= bv[s];
-                    }
-                } else {
-#pragma unroll
-                    for (int s = 0; s < SLOTS; ++s) {
-                        if (tid == 0) u_.scan.pre[s][0] = c;
-                        c *= u_.scan.bp[s][0];
-                    }
+                for (int s = 0; s < SLOTS; ++s) {
+                    if (GATE) s_bp[s][tid] = c;
+                    else if (tid == 0) s_pre0[s] = c;
+                    c *= bv[s];
                 }
                 carry = c;
                 if (lo == 0) write_base_vectors(carry, kx, qx, cs, s_y, s_w, tid);   // carry = Gamma_{1:i}
             }
+            if (lo == 0) wait_vm_all();  // this wave's code copies have landed
             __syncthreads();
             if (GATE) {
                 float P[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) P[j] = u_.scan.pre[ts][8 * l16 + j];
+                for (int j = 0; j < 8; ++j) P[j] = s_bp[ts][SW(l16, j)];
 #pragma unroll
                 for (int q = 0; q < PER_SLOT; ++q) {
                     if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
@@ -289,7 +347,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
                 }
             } else {
                 // scalar decay: one product per slot, applied to the two dot products
-                float P = u_.scan.pre[ts][0];
+                float P = s_pre0[ts];
 #pragma unroll
                 for (int q = 0; q < PER_SLOT; ++q) {
                     if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
@@ -309,7 +367,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
                         acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
                         acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
                     }
-                    P *= R.as[q];
+                    P *= h2f((uint16_t)R.as[q]);
                 }
             }
             if (lo == 0) break;
@@ -324,6 +382,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     // ---- base and token read vectors (written with the last scan when n > 0) -----
     if (n == 0) {
         if (tid < D) write_base_vectors(carry, kx, qx, cs, s_y, s_w, tid);
+        wait_vm_all();
         __syncthreads();
     }
 
@@ -338,7 +397,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             float f[16];
-            decode16<CODE>(zr[m], f);
+            decode16<CODE>(load_codes16<CODE>((const uint8_t *)s_codes + (rg + 32 * m) * ROWB +
+                                              2 * CodeFmt<CODE>::BITS * g8), f);
             float pk = 0.0f, pq = 0.0f;
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
@@ -349,8 +409,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             pq = row8_sum(pq);
             if (g8 == 0) {
                 const int vrow = rg + 32 * m;
-                s_z[0][vrow] = dlt[m] * pk;
-                s_z[1][vrow] = dlt[m] * pq;
+                s_z[0][POS(vrow)] = s_dlt[vrow] * pk;
+                s_z[1][POS(vrow)] = s_dlt[vrow] * pq;
             }
         }
     }
@@ -363,8 +423,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
         float pk = 0.0f, pq = 0.0f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            pk = fmaf(kv[j], s_y[0][8 * l16 + j], pk);
-            pq = fmaf(kv[j], s_y[1][8 * l16 + j], pq);
+            pk = fmaf(kv[j], s_y[0][SW(l16, j)], pk);
+            pq = fmaf(kv[j], s_y[1][SW(l16, j)], pq);
         }
         pk = row16_sum(pk);
         pq = row16_sum(pq);
@@ -374,27 +434,35 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
             acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
         }
     }
-    // the scan buffers are dead since the barrier above; reuse them
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        u_.red[ts][0][8 * l16 + j] = acc_k[j];
-        u_.red[ts][1][8 * l16 + j] = acc_q[j];
+    // sum over the wave's 4 slots in registers, then over the 4 waves in LDS:
+    // lane (rho, l16) holds channels 8 l16 + 2 rho + e, e = 0, 1, stored at
+    // [2 lane + e]
+    {
+        float k0, k1, q0, q1;
+        rows4_reduce_scatter(acc_k, k0, k1);
+        rows4_reduce_scatter(acc_q, q0, q1);
+        const int w = tid >> 6, lane = tid & 63;
+        *(float2 *)&s_red[w][0][2 * lane] = make_float2(k0, k1);
+        *(float2 *)&s_red[w][1][2 * lane] = make_float2(q0, q1);
     }
     __syncthreads();
 
     // ---- combine, correction, output, record ------------------------------------
     if (tid < D) {
+        // position t holds channel 8 (t & 15) + (t >> 4) = 8 l16 + 2 rho + e
+        const int j = tid >> 4, e = j & 1;
+        const int idx = 2 * (16 * (j >> 1) + (tid & 15)) + e;
         float ak = s_z[0][tid], aq = s_z[1][tid];
 #pragma unroll
-        for (int s = 0; s < SLOTS; ++s) {
-            ak += u_.red[s][0][tid];
-            aq += u_.red[s][1][tid];
+        for (int w = 0; w < NT / 64; ++w) {
+            ak += s_red[w][0][idx];
+            aq += s_red[w][1][idx];
         }
         // u_t = fp16(v_t - A^T k_t); the b_t = 0 rule reads nothing (the k-side
         // readouts above are then dead code and compiled out)
         const uint16_t uh = f2h(RULE == LQ_RULE_ADD ? vx : vx - ak);
-        a.rec_u[(rbase + n) * D + tid] = uh;
-        a.o[tvec + tid] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
+        a.rec_u[(rbase + n) * D + ch] = uh;
+        a.o[tvec + ch] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
         if (tid == 0) a.rec_len[tile] = n + 1;
     }
 }
