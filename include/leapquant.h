@@ -71,6 +71,8 @@ extern "C" {
 #define LQ_MAX_WINDOW_GDN 256
 #define LQ_MAX_WINDOW_KDA  64
 #define LQ_MAX_POWER_ITERS 64
+/* Also: batch * heads_v <= 2^30 and batch * heads_v * (heads_v / heads_k) < 2^32
+ * (LQ_EUNSUPPORTED otherwise). */
 
 /* Shape and method parameters (host struct, read at each call). */
 typedef struct {

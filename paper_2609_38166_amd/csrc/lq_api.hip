@@ -46,8 +46,11 @@ int32_t check_dims(const lq_dims *d) {
     const int wmax = d->gate == LQ_GATE_DIAG ? LQ_MAX_WINDOW_KDA : LQ_MAX_WINDOW_GDN;
     if (d->window > wmax) return LQ_EUNSUPPORTED;
     // tile index and per-buffer element counts must fit the kernels' integer types
+    // (the decode maps a tile to its key head as tile * ceil(2^32 / group) >> 32,
+    // exact while tiles * group < 2^32)
     const long long tiles = (long long)d->batch * d->heads_v;
     if (tiles > (1LL << 30)) return LQ_EUNSUPPORTED;
+    if (tiles * (d->heads_v / d->heads_k) >= (1LL << 32)) return LQ_EUNSUPPORTED;
     return LQ_OK;
 }
 

@@ -5,7 +5,8 @@
 //           + U~ (K~^T (Gamma_{1:i} x))                     Compensator Tokens
 //           + sum_{j<i} u_j (k~_j^T (Gamma_{j+1:i} x))      buffered records
 // for x = k_t and x = q_t in one pass over the codes (App. B.2 Eq. (readout),
-// App. B.3 Eq. (smooth-readout)), then forms u_t = fp16(v_t - A^T k_t), the
+// App. B.3 Eq. (smooth-readout)) -- the code product on the matrix cores, see
+// below -- then forms u_t = fp16(v_t - A^T k_t), the
 // output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
 //
@@ -68,8 +69,7 @@ struct DecodeArgs {
     const float *alpha;
     const float *beta;
     float *o;
-    int heads_v;
-    int group;      // heads_v / heads_k
+    uint64_t kv_mul; // ceil(2^32 / group), group = heads_v / heads_k
     int window;
     int n_comp;
     int tiles;
@@ -118,31 +118,60 @@ __device__ __forceinline__ void rows4_reduce_scatter(const float *x, float &s0, 
     s1 = __uint_as_float(r1[0]) + __uint_as_float(r1[1]);
 }
 
-// y = Gamma_{1:i} x (swizzled) and w = c . y (channel order) for x = k_t, q_t;
-// thread t < D: channel CH(t).
+// The read vectors of the code product, w = c . Gamma_{1:i} x, as three bf16
+// parts with w = hi + mid + lo exactly: hi and mid keep the leading 8
+// significant bits of w and of w - hi (truncation, so both differences are
+// exact in fp32), and the remainder has at most 8 significant bits left.
+// s_wb[part][0 = k_t, 1 = q_t][channel], bf16 bits.
+__device__ __forceinline__ void split_bf16x3(float w, uint16_t (*s_wb)[2][D], int vec, int c) {
+    const uint32_t hi = __float_as_uint(w) & 0xFFFF0000u;
+    const float r1 = w - __uint_as_float(hi);
+    const uint32_t mid = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(mid);
+    s_wb[0][vec][c] = (uint16_t)(hi >> 16);
+    s_wb[1][vec][c] = (uint16_t)(mid >> 16);
+    s_wb[2][vec][c] = f2bf(r2);
+}
+
+// y = Gamma_{1:i} x (swizzled) and the split of w = c . y (channel order) for
+// x = k_t, q_t; thread t < D: channel CH(t).
 __device__ __forceinline__ void write_base_vectors(float G, float kx, float qx, float cs, float (*s_y)[D],
-                                                   float (*s_w)[D], int t) {
+                                                   uint16_t (*s_wb)[2][D], int t) {
     const float yk = G * kx, yq = G * qx;
     s_y[0][t] = yk;
     s_y[1][t] = yq;
-    s_w[0][CH(t)] = cs * yk;
-    s_w[1][CH(t)] = cs * yq;
+    split_bf16x3(cs * yk, s_wb, 0, CH(t));
+    split_bf16x3(cs * yq, s_wb, 1, CH(t));
 }
 
-// 16 consecutive codes of a row: 16 bytes (byte formats), 8 (INT4) or 12 (INT6).
+// Code rows in LDS are stored in 16-byte chunks, each row rotated by zrot(v)
+// chunks, so that the 16 rows a matrix-core operand reads at one chunk
+// position fall in distinct banks.  The rotation is applied when the copy is
+// issued (lane L's destination is fixed; its source chunk is chosen).  The
+// 6-bit rows (96 bytes, 16 codes = 12 bytes) are not rotated.
+template <int CODE> __device__ __forceinline__ int zrot(int v) {
+    return CODE == 3 ? 0 : (CODE == 2 ? (v >> 2) & 3 : (v >> 1) & 7);
+}
+
+// Codes 16 s .. 16 s + 15 of row v from the rotated LDS copy.
 template <int CODE>
-__device__ __forceinline__ uint4 load_codes16(const uint8_t *p) {
-    if (CODE <= 1) return *(const uint4 *)p;
+__device__ __forceinline__ uint4 lds_codes16(const uint4 *z, int v, int s) {
+    constexpr int SEGS = D * CodeFmt<CODE>::BITS / 8 / 16;     // chunks per row
+    if (CODE <= 1) return z[v * SEGS + ((s + zrot<CODE>(v)) & (SEGS - 1))];
     if (CODE == 2) {
-        const uint2 w = *(const uint2 *)p;
+        const uint2 *h = (const uint2 *)&z[v * SEGS + (((s >> 1) + zrot<CODE>(v)) & (SEGS - 1))];
+        const uint2 w = h[s & 1];
         return make_uint4(w.x, w.y, 0u, 0u);
     }
-    const uint32_t *w = (const uint32_t *)p;
+    const uint32_t *w = (const uint32_t *)((const uint8_t *)z + v * (SEGS * 16) + 12 * s);
     return make_uint4(w[0], w[1], w[2], 0u);
 }
 
-// Issue the loads of the records in [lo, hi) that belong to slot ts: record
-// hi-1-(PER_SLOT*ts+q) goes to register set q (newest first).
+// bf16 bits of two small exact floats, packed low | high << 16.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+}
+
 template <int GATE>
 __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi,
                                              int ts, int l16, RecRegs<GATE> &R) {
@@ -166,7 +195,7 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     constexpr int ZCH = D * ROWB / 16;                   // 16-byte chunks of a tile's codes
     static_assert(ZCH % NT == 0, "whole chunks per thread");
     __shared__ float s_x[2][D];          // x = k_t, q_t (swizzled)
-    __shared__ float s_w[2][D];          // c . Gamma_{1:i} . x (channel order)
+    __shared__ __align__(16) uint16_t s_wb[3][2][D];   // c . Gamma_{1:i} . x as bf16 parts
     __shared__ float s_y[2][D];          // Gamma_{1:i} . x (swizzled)
     __shared__ float s_z[2][D];          // quantized-residual readout (swizzled)
     __shared__ float s_kq[2];            // k~_t . q_t (per wave pair)
@@ -182,14 +211,15 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
 
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
-    const int b = tile / a.heads_v, hv = tile - b * a.heads_v;
-    const size_t kvec = ((size_t)b * (a.heads_v / a.group) + hv / a.group) * D;
+    // tile = b H_v + h_v and H_v = H_k group, so the key/query head row is
+    // b H_k + h_v / group = tile / group, taken as a multiply by ceil(2^32 /
+    // group) and a shift (exact while tiles * group < 2^32, which the launch
+    // checks)
+
     const size_t tvec = (size_t)tile * D;
 
     const int l16 = tid & 15;            // 8-channel key segment / 8-value segment
     const int ts = tid >> 4;             // slot 0..15
-    const int g8 = tid & 7;              // 16-channel key segment of the code rows
-    const int rg = tid >> 3;             // code rows rg, rg+32, rg+64, rg+96
     const size_t rbase = (size_t)tile * a.window;
 
     // ---- issue every load of the tile: rec_len (a scalar load, which the record
@@ -200,20 +230,35 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     // (beta, and alpha of the scalar gate, are per-tile scalars)
     float bt = a.beta[tile];
     float al = GATE ? 0.0f : a.alpha[tile];
+    // The token pointers are pinned here so that their kernel-argument loads
+    // join the others at the top instead of being sunk into the branch below
+    // behind a second wait.
+    // (cast back to the global address space: out of the asm they are generic
+    // pointers, which would be read with flat loads)
+    const float *pk = a.k, *pq = a.q, *pc = a.smooth, *pa = a.alpha, *pv = a.v;
+    uint64_t kvm = a.kv_mul;
+    asm volatile("" : "+s"(pk), "+s"(pq), "+s"(pc), "+s"(pa), "+s"(pv), "+s"(kvm));
+    using gf = const __attribute__((address_space(1))) float;
+    const size_t kvec = (size_t)(((uint64_t)(uint32_t)tile * kvm) >> 32) * D;
     float kx = 0.0f, qx = 0.0f, cs = 0.0f, vx = 0.0f;
     if (tid < D) {
-        kx = a.k[kvec + ch];
-        qx = a.q[kvec + ch];
-        cs = a.smooth[tvec + ch];
-        if (GATE) al = a.alpha[tvec + ch];
-        vx = a.v[tvec + ch];
+        kx = ((gf *)pk)[kvec + ch];
+        qx = ((gf *)pq)[kvec + ch];
+        cs = ((gf *)pc)[tvec + ch];
+        if (GATE) al = ((gf *)pa)[tvec + ch];
+        vx = ((gf *)pv)[tvec + ch];
     }
     {
-        // chunk c = NT m + 64 w + L goes to s_codes[c]: wave w's lanes fill 1 KiB
+        // LDS chunk P = NT m + 64 w + L (wave w's lanes fill 1 KiB) holds chunk
+        // (P - zrot(v)) mod SEGS of row v = P / SEGS
+        constexpr int SEGS = ROWB / 16;
         const uint4 *zt = (const uint4 *)(a.codes + (size_t)tile * D * ROWB);
         const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
-        for (int m = 0; m < ZCH / NT; ++m) dma16(zt + NT * m + tid, lds_addr(&s_codes[NT * m + 64 * w]));
+        for (int m = 0; m < ZCH / NT; ++m) {
+            const int P = NT * m + tid, v = P / SEGS, c = P - v * SEGS;
+            dma16(zt + v * SEGS + ((c - zrot<CODE>(v) + SEGS) % SEGS), lds_addr(&s_codes[NT * m + 64 * w]));
+        }
     }
     if (tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(s_dlt));   // per-row scales, wave 0
     uint4 ck = make_uint4(0, 0, 0, 0), cu = make_uint4(0, 0, 0, 0);
@@ -310,7 +355,7 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
                     c *= bv[s];
                 }
                 carry = c;
-                if (lo == 0) write_base_vectors(carry, kx, qx, cs, s_y, s_w, tid);   // carry = Gamma_{1:i}
+                if (lo == 0) write_base_vectors(carry, kx, qx, cs, s_y, s_wb, tid);   // carry = Gamma_{1:i}
             }
             if (lo == 0) wait_vm_all();  // this wave's code copies have landed
             __syncthreads();
@@ -381,37 +426,65 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
 
     // ---- base and token read vectors (written with the last scan when n > 0) -----
     if (n == 0) {
-        if (tid < D) write_base_vectors(carry, kx, qx, cs, s_y, s_w, tid);
+        if (tid < D) write_base_vectors(carry, kx, qx, cs, s_y, s_wb, tid);
         wait_vm_all();
         __syncthreads();
     }
 
-    // ---- quantized residual: rows rg + 32m, channels 16*g8 .. +15 ---------------
+    // ---- quantized residual on the matrix cores ----------------------------------
+    // Per 16-row block of wave w's 32 rows: D (16 rows x 16 columns) = A (rows x
+    // 32 channels of codes, in bf16: every code is a small exact value) times B
+    // (32 channels x columns; column j reads vector j & 1, only columns 0 (k_t)
+    // and 1 (q_t) are kept), with the three bf16 parts of w stacked along the
+    // contraction so the matrix core adds them; fp32 accumulation.  Lane (i, g)
+    // of an operand holds row / column i and 8 channels of group g; the channel
+    // order inside the contraction is free as long as A and B agree: lane g's
+    // 16-code segment s = 4p + g supplies its 8 channels of virtual block 2p
+    // (codes 16s..16s+7) and 2p + 1 (16s+8..16s+15).
     {
-        float wk[16], wq[16];
+        typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        const int lane = tid & 63, i16 = lane & 15, g = lane >> 4, wv = tid >> 6;
+        // one accumulator per row block and part: dependent chains of 4
+        f32x4 acc[2][3];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            wk[j] = s_w[0][16 * g8 + j];
-            wq[j] = s_w[1][16 * g8 + j];
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int part = 0; part < 3; ++part) acc[rb][part] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            const int seg = 4 * pp + g;
+            bf16x8 bw[2][3];
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int part = 0; part < 3; ++part)
+                    bw[h][part] = *(const bf16x8 *)&s_wb[part][i16 & 1][16 * seg + 8 * h];
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                float f[16];
+                decode16<CODE>(lds_codes16<CODE>(s_codes, 32 * wv + 16 * rb + i16, seg), f);
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t av[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) av[e] = pack_bf16x2(f[8 * h + 2 * e], f[8 * h + 2 * e + 1]);
+                    const bf16x8 A8 = __builtin_bit_cast(bf16x8, make_uint4(av[0], av[1], av[2], av[3]));
+#pragma unroll
+                    for (int part = 0; part < 3; ++part)
+                        acc[rb][part] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A8, bw[h][part], acc[rb][part], 0, 0, 0);
+                }
+            }
         }
+        // column i16 (< 2), rows 4 g + r of each block
+        if (i16 < 2) {
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            float f[16];
-            decode16<CODE>(load_codes16<CODE>((const uint8_t *)s_codes + (rg + 32 * m) * ROWB +
-                                              2 * CodeFmt<CODE>::BITS * g8), f);
-            float pk = 0.0f, pq = 0.0f;
+            for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                pk = fmaf(f[j], wk[j], pk);
-                pq = fmaf(f[j], wq[j], pq);
-            }
-            pk = row8_sum(pk);
-            pq = row8_sum(pq);
-            if (g8 == 0) {
-                const int vrow = rg + 32 * m;
-                s_z[0][POS(vrow)] = s_dlt[vrow] * pk;
-                s_z[1][POS(vrow)] = s_dlt[vrow] * pq;
-            }
+                for (int r = 0; r < 4; ++r) {
+                    const int vrow = 32 * wv + 16 * rb + 4 * g + r;
+                    s_z[i16][POS(vrow)] = s_dlt[vrow] * ((acc[rb][0][r] + acc[rb][1][r]) + acc[rb][2][r]);
+                }
         }
     }
 
@@ -496,8 +569,8 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
     a.alpha = t.alpha;
     a.beta = t.beta;
     a.o = t.o;
-    a.heads_v = d.heads_v;
-    a.group = d.heads_v / d.heads_k;
+    const uint64_t group = (uint64_t)(d.heads_v / d.heads_k);
+    a.kv_mul = ((1ull << 32) + group - 1) / group;
     a.window = d.window;
     a.n_comp = d.n_comp;
     a.tiles = d.batch * d.heads_v;

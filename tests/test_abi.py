@@ -78,6 +78,10 @@ def test_validation_rejects_bad_arguments_before_launch():
         dd = B.make_dims(2, 4, heads_k=2, **kw)
         assert _call_decode(dd, st, toks) == code, kw
     assert _call_decode(B.make_dims(2, 4, heads_k=3), st, toks) == B.LQ_EINVAL
+    # size limits: batch * heads_v <= 2^30, and batch * heads_v * group < 2^32
+    assert _call_decode(B.make_dims(1 << 26, 32, heads_k=32), st, toks) == B.LQ_EUNSUPPORTED
+    assert _call_decode(B.make_dims(1 << 20, 256, heads_k=4), st, toks) == B.LQ_EUNSUPPORTED
+    assert _call_decode(B.make_dims(1 << 20, 256, heads_k=128), st, toks) != B.LQ_EUNSUPPORTED
     L = B.lib()
     assert L.leapquant_baseline_step(C.byref(d), good, 7, *toks, None) == B.LQ_EINVAL
     assert L.leapquant_window_commit(C.byref(d), C.byref(st), good + 8, None) == B.LQ_EALIGN
