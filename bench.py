@@ -274,6 +274,55 @@ def per_launch_times(wl, dims, S0, toks, reps=3):
                                                    ("quantize_ms", res["quantize"]))}
 
 
+def decode_two_batches(wl, dims, S0, toks, reps=3):
+    """Average decode launch duration when two independent batches of the same
+    size alternate launch by launch (positions 1..W each, one graph): the other
+    batch's codes evict this batch's from the 256 MB Infinity Cache, so the
+    codes come from HBM on every step.  In the single-batch loop a batch's
+    int8 codes (134 MB at 8192 tiles) can stay resident from one step to the
+    next; this figure is the decode without that help."""
+    import torch
+    from paper_2609_38166_amd import binding as B_
+    sts = [B_.State.empty(dims) for _ in range(2)]
+    o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+    q, k, v, a, b = toks
+    W = wl.window
+
+    def window():
+        for i in range(W):
+            for st in sts:
+                B_.leapquant_decode_step(dims, st, q[i], k[i], v[i], a[i], b[i], o)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for st in sts:
+            B_.leapquant_quantize_state(dims, S0, st)
+        window()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        window()
+    torch.cuda.synchronize()
+    ts = []
+    for rep in range(reps + 1):
+        for st in sts:
+            B_.leapquant_quantize_state(dims, S0, st)      # rec_len := 0
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if rep:
+            ts.append(e0.elapsed_time(e1) / (2 * W))
+    for st in sts:
+        if B_.leapquant_check_error(st):
+            raise RuntimeError("device error during the two-batch decode timing")
+    del sts
+    return float(np.mean(ts))
+
+
 def copy_calibration(nbytes=1 << 30):
     """One plain device-to-device copy of known size, for scaling the HBM byte
     counters of a profiler run (FETCH_SIZE / WRITE_SIZE of this dispatch are
@@ -285,6 +334,40 @@ def copy_calibration(nbytes=1 << 30):
     dst.copy_(src)
     torch.cuda.synchronize()
     del src, dst
+
+
+def stream_read_ceiling(nbytes=4 << 30, reps=5):
+    """Measured HBM read rate of a kernel that only streams a 4 GiB buffer
+    (non-temporal 16-byte coalesced loads, far beyond the 256 MB Infinity
+    Cache): the practical read ceiling next to which the decode's rate is read."""
+    import ctypes as C
+    import torch
+    from paper_2609_38166_amd import build as lib_build
+    L = C.CDLL(lib_build.BENCH_LIB)
+    L.lqb_stream_read.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int, C.c_void_p]
+    L.lqb_stream_read.restype = C.c_int
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    grid = 256 * 128
+    sink = torch.empty(grid, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def launch():
+        rc = L.lqb_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"lqb_stream_read failed: {rc}")
+    launch()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        launch()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    del buf, sink
+    gbs = nbytes / float(np.median(ts)) / 1e9
+    return {"gbps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes}
 
 
 def traffic_from_profile(wl):
@@ -464,6 +547,16 @@ def main():
                        "commit": round(kt["commit_ms"] * 1e3, 2),
                        "quantize": round(kt["quantize_ms"] * 1e3, 2)},
     }
+
+    two = decode_two_batches(wl, dims, S0, toks)
+    out["roofline"]["two_batch_decode"] = {
+        "avg_launch_us": round(two * 1e3, 2), "achieved": round(dec_avg_bytes / (two * 1e-3) / 1e9, 1),
+        "note": "two batches alternate, so no batch's codes stay in the Infinity Cache between its steps"}
+    log(f"[bench] decode with two alternating batches {two * 1e3:.1f} us/launch")
+    ceil = stream_read_ceiling()
+    out["stream_read_ceiling"] = ceil
+    out["roofline"]["frac_of_stream_ceiling"] = round(achieved / ceil["gbps"], 4)
+    log(f"[bench] streaming-read ceiling {ceil}")
 
     if not args.no_variants and wl.name == "kda_kimi":
         # the same layer with the paper's lower-bit residual codes (same inputs)

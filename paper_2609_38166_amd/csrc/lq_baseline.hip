@@ -13,6 +13,29 @@ namespace lq {
 
 namespace {
 
+// State accesses.  The bf16 state is streamed with non-temporal loads and
+// stores (measured 6% faster per step than plain accesses at 8192 tiles); the
+// fp32 state is faster with plain ones (non-temporal stores cost it 1.6x).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+template <bool NT>
+__device__ __forceinline__ uint4 ld_state16(const uint4 *p) {
+    if (NT) {
+        const u32x4_t v = __builtin_nontemporal_load((const u32x4_t *)p);
+        return make_uint4(v.x, v.y, v.z, v.w);
+    }
+    return *p;
+}
+template <bool NT>
+__device__ __forceinline__ void st_state16(uint4 *p, uint4 w) {
+    if (NT) {
+        const u32x4_t v = {w.x, w.y, w.z, w.w};
+        __builtin_nontemporal_store(v, (u32x4_t *)p);
+    } else {
+        *p = w;
+    }
+}
+
+
 struct BaseArgs {
     void *S;
     const float *q;
@@ -64,7 +87,7 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
         const uint16_t *St = (const uint16_t *)a.S + (size_t)tile * D * D;
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
-            const uint4 p = *(const uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
+            const uint4 p = ld_state16<BF16 != 0>((const uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16));
             const uint32_t w[4] = {p.x, p.y, p.z, p.w};
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -76,8 +99,10 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
         const float *St = (const float *)a.S + (size_t)tile * D * D;
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
-            const float4 *row = (const float4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
-            const float4 lo = row[0], hi = row[1];
+            const uint4 *row = (const uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
+            const uint4 lo_ = ld_state16<BF16 != 0>(row), hi_ = ld_state16<BF16 != 0>(row + 1);
+            const float4 lo = make_float4(__uint_as_float(lo_.x), __uint_as_float(lo_.y), __uint_as_float(lo_.z), __uint_as_float(lo_.w));
+            const float4 hi = make_float4(__uint_as_float(hi_.x), __uint_as_float(hi_.y), __uint_as_float(hi_.z), __uint_as_float(hi_.w));
             s[m][0] = lo.x; s[m][1] = lo.y; s[m][2] = lo.z; s[m][3] = lo.w;
             s[m][4] = hi.x; s[m][5] = hi.y; s[m][6] = hi.z; s[m][7] = hi.w;
         }
@@ -115,15 +140,15 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
             w.y = f2bf(s[m][2]) | ((uint32_t)f2bf(s[m][3]) << 16);
             w.z = f2bf(s[m][4]) | ((uint32_t)f2bf(s[m][5]) << 16);
             w.w = f2bf(s[m][6]) | ((uint32_t)f2bf(s[m][7]) << 16);
-            *(uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16) = w;
+            st_state16<BF16 != 0>((uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16), w);
         }
     } else {
         float *St = (float *)a.S + (size_t)tile * D * D;
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
-            float4 *row = (float4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
-            row[0] = make_float4(s[m][0], s[m][1], s[m][2], s[m][3]);
-            row[1] = make_float4(s[m][4], s[m][5], s[m][6], s[m][7]);
+            uint4 *row = (uint4 *)(St + (size_t)(r0 + 16 * m) * D + 8 * l16);
+            st_state16<BF16 != 0>(row, make_uint4(__float_as_uint(s[m][0]), __float_as_uint(s[m][1]), __float_as_uint(s[m][2]), __float_as_uint(s[m][3])));
+            st_state16<BF16 != 0>(row + 1, make_uint4(__float_as_uint(s[m][4]), __float_as_uint(s[m][5]), __float_as_uint(s[m][6]), __float_as_uint(s[m][7])));
         }
     }
 }
