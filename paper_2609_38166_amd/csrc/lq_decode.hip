@@ -10,12 +10,13 @@
 // output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
 //
-// Every global load of the tile is issued before the first barrier, those that
-// do not depend on rec_len first: the token inputs, the d_v x d_k codes (copied
-// straight into LDS, 16 bytes per lane and instruction, so they hold no
-// registers), the compensators, then rec_len and one pass of records (16 slots
-// of 16 lanes, each slot a contiguous block of records, 16 bytes of key,
-// correction and decay per lane).  The decays
+// Every global load of the tile is issued before the first barrier: rec_len (a
+// scalar load, which the record loads wait for), the token inputs, the
+// d_v x d_k codes and row scales (copied straight into LDS, 16 bytes per lane
+// and instruction, so they hold no registers), the compensators, then one pass
+// of records, loaded non-temporally (16 slots of 16 lanes, each slot a
+// contiguous block of records, 16 bytes of key, correction and decay per
+// lane).  The decays
 // Gamma_{j+1:i} are products of the FP16 record decays: each slot forms the
 // product of its block, one scan over the 16 slots gives every block the decay
 // of all newer records, and the slot walks its block from the newest record
@@ -29,13 +30,10 @@ namespace {
 
 constexpr int SLOTS = 16;            // 16-lane groups per workgroup
 // Records per slot and pass: the diagonal gate carries a 16-byte decay per lane
-// and record, so it holds PS_DIAG per slot to stay within 128 VGPRs (4 resident
-// workgroups per CU); the scalar gate holds four (64 per pass).
-#ifndef LQ_PS_DIAG
-#define LQ_PS_DIAG 3
-#endif
+// and record, so it holds three per slot (48 per pass) to stay within 128
+// VGPRs (4 resident workgroups per CU); the scalar gate holds four (64 per pass).
 template <int GATE> struct Pass {
-    static constexpr int PER_SLOT = GATE ? LQ_PS_DIAG : 4;
+    static constexpr int PER_SLOT = GATE ? 3 : 4;
     static constexpr int N = SLOTS * PER_SLOT;
 };
 
