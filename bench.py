@@ -559,6 +559,27 @@ def main():
     log(f"[bench] streaming-read ceiling {ceil}")
 
     if not args.no_variants and wl.name == "kda_kimi":
+        # One GPU's share under 8-way tensor parallelism (heads split across GPUs):
+        # the first heads_v / 8 heads of every request, 1024 tiles -- a single
+        # round of resident decode workgroups, so occupancy and the tail differ.
+        sw = wl.with_(name="kda_kimi_tp8_shard", heads_v=wl.heads_v // 8, heads_k=wl.heads_k // 8)
+        sd = B_.make_dims(sw.batch, sw.heads_v, sw.heads_k, window=sw.window, n_comp=sw.n_comp,
+                          power_iters=sw.power_iters, gate=sw.gate, code=sw.code)
+        s_S0 = S0[:, :sw.heads_v].contiguous()
+        s_toks = tuple(t_[:W, :, :(sw.heads_k if j < 2 else sw.heads_v)].contiguous()
+                       for j, t_ in enumerate(toks))
+        sk = per_launch_times(sw, sd, s_S0, s_toks)
+        sstep = sk["decode_ms"] * sw.steps + sk["commit_ms"] * (sw.steps // W) + sk["quantize_ms"]
+        sbytes = float(np.mean([decode_bytes(sw, i) for i in range(1, W + 1)])) * sw.tiles
+        out["tp8_shard"] = {"tiles": sw.tiles, "heads_v": sw.heads_v,
+                            "value_from_kernels": round(sw.tiles * sw.steps / (sstep * 1e-3), 1),
+                            "decode_us": round(sk["decode_ms"] * 1e3, 2),
+                            "decode_gbps": round(sbytes / (sk["decode_ms"] * 1e-3) / 1e9, 1),
+                            "commit_us": round(sk["commit_ms"] * 1e3, 2),
+                            "quantize_us": round(sk["quantize_ms"] * 1e3, 2)}
+        log(f"[bench] tp8 shard: {out['tp8_shard']}")
+        del s_S0, s_toks
+
         # the same layer with the paper's lower-bit residual codes (same inputs)
         var = {}
         for vname in ("kda_kimi_int6", "kda_kimi_int4"):
