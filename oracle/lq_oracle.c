@@ -19,7 +19,10 @@
  *       instance table (App. A): A = D_t S, u = v - A^T k, S = A + beta k u^T,
  *       o = S^T q.  The rows with b_t = 0 (linear attention, RetNet, Mamba2,
  *       GLA / RWKV6 / HGRN2) drop the read: u = v (cfg->rule = 1).  Because the read vector is b = alpha k (GDN) or alpha.k
- *       (KDA) and D_t is diagonal, S_{t-1}^T b = (D_t S_{t-1})^T k.
+ *       (KDA) and D_t is diagonal, S_{t-1}^T b = (D_t S_{t-1})^T k.  With
+ *       cfg->rule = 2 the read vector is an input of its own, u = v - S_{t-1}^T b
+ *       (the general form, App. A; the erase sub-step of RWKV7, whose read
+ *       vector a.kappa is not the decay times the write key).
  *   O2  quantizer: Compensator Tokens (Sec. 3.3, Eqs. (compensator),
  *       (compensator-rank-r)), fitted by power iteration (Sec. 4.1), then
  *       residual smoothing (Sec. 3.4) and per-value-channel symmetric INT8
@@ -69,7 +72,8 @@ typedef struct {
     int32_t smooth;        /* 1: residual smoothing; 0: c = 1 */
     int32_t quantize;      /* 1: quantize at window ends; 0: keep the state exact */
     int32_t round_records; /* 1: FP16 records (alpha, write key, correction); 0: exact */
-    int32_t rule;          /* 0: delta rule (b_t = D_t k_t); 1: additive (b_t = 0) */
+    int32_t rule;          /* 0: delta rule (b_t = D_t k_t); 1: additive (b_t = 0);
+                            * 2: general, b_t given with the token */
 } lqo_cfg;
 
 enum { LQO_STATE_EXACT = 0, LQO_STATE_F32 = 1, LQO_STATE_BF16 = 2 };
@@ -261,20 +265,27 @@ static real state_round(int mode, real x)
 }
 
 static void recurrent_step_impl(const lqo_cfg *cfg, real *S, const float *q, const float *k,
-                                const float *vv, const float *alpha, float beta, double *o,
-                                int mode, real *w)
+                                const float *b, const float *vv, const float *alpha, float beta,
+                                double *o, int mode, real *w)
 {
     const int dk = cfg->dk, dv = cfg->dv;
+    if (cfg->rule == 2)
+        for (int v = 0; v < dv; ++v) {
+            real s = 0;
+            for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)b[i];  /* S_{t-1}^T b */
+            w[v] = (real)vv[v] - s;                                         /* u */
+        }
     for (int i = 0; i < dk; ++i) {
         real a = (real)alpha[cfg->gate ? i : 0];
         for (int v = 0; v < dv; ++v) S[i * dv + v] *= a;                   /* A = D S */
     }
-    for (int v = 0; v < dv; ++v) {
-        real s = 0;
-        if (cfg->rule == 0)
-            for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];  /* A^T k */
-        w[v] = (real)vv[v] - s;                                             /* u */
-    }
+    if (cfg->rule != 2)
+        for (int v = 0; v < dv; ++v) {
+            real s = 0;
+            if (cfg->rule == 0)
+                for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];  /* A^T k */
+            w[v] = (real)vv[v] - s;                                             /* u */
+        }
     for (int i = 0; i < dk; ++i) {
         real wk = (real)beta * (real)k[i];                                  /* beta k */
         for (int v = 0; v < dv; ++v) S[i * dv + v] += wk * w[v];
@@ -288,13 +299,14 @@ static void recurrent_step_impl(const lqo_cfg *cfg, real *S, const float *q, con
 }
 
 void OQ(recurrent_step)(const lqo_cfg *cfg, double *S, const float *q, const float *k,
-                        const float *v, const float *alpha, float beta, double *o, int mode)
+                        const float *b, const float *v, const float *alpha, float beta, double *o,
+                        int mode)
 {
     const int n = cfg->dk * cfg->dv;
     real *Sr = (real *)malloc(sizeof(real) * (size_t)n);
     real *w = (real *)malloc(sizeof(real) * (size_t)cfg->dv);
     for (int i = 0; i < n; ++i) Sr[i] = (real)S[i];
-    recurrent_step_impl(cfg, Sr, q, k, v, alpha, beta, o, mode, w);
+    recurrent_step_impl(cfg, Sr, q, k, b, v, alpha, beta, o, mode, w);
     for (int i = 0; i < n; ++i) S[i] = (double)Sr[i];
     free(Sr);
     free(w);
@@ -307,22 +319,30 @@ void OQ(recurrent_step)(const lqo_cfg *cfg, double *S, const float *q, const flo
 /* ------------------------------------------------------------------------ */
 
 static void window_step_impl(const lqo_cfg *cfg, real *S, const float *q, const float *k,
-                             const float *vv, const float *alpha, float beta, double *o,
-                             double *ra, double *rk, double *ru, real *u)
+                             const float *b, const float *vv, const float *alpha, float beta,
+                             double *o, double *ra, double *rk, double *ru, real *u)
 {
     const int dk = cfg->dk, dv = cfg->dv, g = cfg->gate ? dk : 1;
     for (int i = 0; i < g; ++i) ra[i] = (double)rec_round(cfg, (real)alpha[i]);
+    if (cfg->rule == 2)
+        for (int v = 0; v < dv; ++v) {
+            real s = 0;
+            for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)b[i];
+            u[v] = rec_round(cfg, (real)vv[v] - s);                         /* u_i = v_i - S_{i-1}^T b_i */
+            ru[v] = (double)u[v];
+        }
     for (int i = 0; i < dk; ++i) {
         real a = (real)ra[cfg->gate ? i : 0];
         for (int v = 0; v < dv; ++v) S[i * dv + v] *= a;                   /* A_i = D_i S_{i-1} */
     }
-    for (int v = 0; v < dv; ++v) {
-        real s = 0;
-        if (cfg->rule == 0)
-            for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];
-        u[v] = rec_round(cfg, (real)vv[v] - s);                             /* u_i = v_i - A_i^T k_i */
-        ru[v] = (double)u[v];
-    }
+    if (cfg->rule != 2)
+        for (int v = 0; v < dv; ++v) {
+            real s = 0;
+            if (cfg->rule == 0)
+                for (int i = 0; i < dk; ++i) s += S[i * dv + v] * (real)k[i];
+            u[v] = rec_round(cfg, (real)vv[v] - s);                         /* u_i = v_i - A_i^T k_i */
+            ru[v] = (double)u[v];
+        }
     for (int i = 0; i < dk; ++i) {
         /* beta*k as an fp32 product, the precision of the inputs */
         real tk = cfg->round_records ? f16v((real)(beta * k[i])) : (real)beta * (real)k[i];
@@ -337,14 +357,14 @@ static void window_step_impl(const lqo_cfg *cfg, real *S, const float *q, const 
 }
 
 void OQ(window_step)(const lqo_cfg *cfg, double *S, const float *q, const float *k,
-                     const float *v, const float *alpha, float beta, double *o, double *ra,
-                     double *rk, double *ru)
+                     const float *b, const float *v, const float *alpha, float beta, double *o,
+                     double *ra, double *rk, double *ru)
 {
     const int n = cfg->dk * cfg->dv;
     real *Sr = (real *)malloc(sizeof(real) * (size_t)n);
     real *u = (real *)malloc(sizeof(real) * (size_t)cfg->dv);
     for (int i = 0; i < n; ++i) Sr[i] = (real)S[i];
-    window_step_impl(cfg, Sr, q, k, v, alpha, beta, o, ra, rk, ru, u);
+    window_step_impl(cfg, Sr, q, k, b, v, alpha, beta, o, ra, rk, ru, u);
     for (int i = 0; i < n; ++i) S[i] = (double)Sr[i];
     free(Sr);
     free(u);
@@ -407,8 +427,8 @@ static void readout_impl(const lqo_cfg *cfg, const uint8_t *Z, const float *delt
 void OQ(readout_step)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, const float *c,
                       const double *Kt, const double *Ut, const double *S0, const double *rec_a,
                       const double *rec_k, const double *rec_u, int n_rec, const float *q,
-                      const float *k, const float *vv, const float *alpha, float beta, double *o,
-                      double *na, double *nk, double *nu)
+                      const float *k, const float *b, const float *vv, const float *alpha,
+                      float beta, double *o, double *na, double *nk, double *nu)
 {
     const int dk = cfg->dk, dv = cfg->dv, g = cfg->gate ? dk : 1;
     real *Ak = (real *)malloc(sizeof(real) * (size_t)dv);
@@ -418,8 +438,13 @@ void OQ(readout_step)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, 
     for (int i = 0; i < g; ++i) na[i] = (double)rec_round(cfg, (real)alpha[i]);
     const int ell = n_rec + 1;
     /* A_i^T x = S_{i-1}^T (Gamma_{i:i} x): the base and all records decay
-     * through token i, none of the records includes token i itself. */
-    readout_impl(cfg, Z, delta, c, Kt, Ut, S0, rec_a, rec_k, rec_u, n_rec, na, ell, n_rec, k, Ak, y, xg);
+     * through token i, none of the records includes token i itself.  The
+     * general rule reads S_{i-1}^T b instead: the same sum with the decays of
+     * the records only (ell = n_rec). */
+    if (cfg->rule == 2)
+        readout_impl(cfg, Z, delta, c, Kt, Ut, S0, rec_a, rec_k, rec_u, n_rec, na, n_rec, n_rec, b, Ak, y, xg);
+    else
+        readout_impl(cfg, Z, delta, c, Kt, Ut, S0, rec_a, rec_k, rec_u, n_rec, na, ell, n_rec, k, Ak, y, xg);
     readout_impl(cfg, Z, delta, c, Kt, Ut, S0, rec_a, rec_k, rec_u, n_rec, na, ell, n_rec, q, Aq, y, xg);
     real kq = 0;
     for (int i = 0; i < dk; ++i) {
@@ -428,7 +453,7 @@ void OQ(readout_step)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, 
         kq += tk * (real)q[i];
     }
     for (int v = 0; v < dv; ++v) {
-        real u = rec_round(cfg, (real)vv[v] - (cfg->rule == 0 ? Ak[v] : (real)0));
+        real u = rec_round(cfg, (real)vv[v] - (cfg->rule == 1 ? (real)0 : Ak[v]));
         nu[v] = (double)u;
         o[v] = (double)(Aq[v] + u * kq);                                     /* S_i^T q */
     }
@@ -501,7 +526,13 @@ typedef struct {
     const float *v;     /* [tiles][T][dv] */
     const float *alpha; /* [tiles][T][g] */
     const float *beta;  /* [tiles][T] */
+    const float *b;     /* [tiles][T][dk] read vectors (rule 2 only; may be NULL otherwise) */
 } lqo_inputs;
+
+static const float *read_vec(const lqo_inputs *in, size_t ts, int dk)
+{
+    return in->b ? in->b + ts * dk : NULL;
+}
 
 static int n_snap_of(const lqo_cfg *cfg, int T) { return 1 + T / cfg->window; }
 
@@ -557,8 +588,8 @@ int OQ(run_dense)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
         int n = 0;
         for (int s = 0; s < T; ++s) {
             const size_t ts = (size_t)t * T + s;
-            window_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, in->v + ts * dv,
-                             in->alpha + ts * g, in->beta[ts], o + ts * dv, ra + (size_t)n * g,
+            window_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, read_vec(in, ts, dk),
+                             in->v + ts * dv, in->alpha + ts * g, in->beta[ts], o + ts * dv, ra + (size_t)n * g,
                              rk + (size_t)n * dk, ru + (size_t)n * dv, u);
             store_hist(cfg, out, ts, ra + (size_t)n * g, rk + (size_t)n * dk, ru + (size_t)n * dv);
             if (++n == W) {
@@ -619,8 +650,8 @@ int OQ(run_readout)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
         for (int s = 0; s < T; ++s) {
             const size_t ts = (size_t)t * T + s;
             OQ(readout_step)(cfg, cfg->quantize ? Z : NULL, delta, c, Kt, Ut, Sd, ra, rk, ru, n,
-                             in->q + ts * dk, in->k + ts * dk, in->v + ts * dv, in->alpha + ts * g,
-                             in->beta[ts], o + ts * dv, ra + (size_t)n * g, rk + (size_t)n * dk,
+                             in->q + ts * dk, in->k + ts * dk, read_vec(in, ts, dk), in->v + ts * dv,
+                             in->alpha + ts * g, in->beta[ts], o + ts * dv, ra + (size_t)n * g, rk + (size_t)n * dk,
                              ru + (size_t)n * dv);
             store_hist(cfg, out, ts, ra + (size_t)n * g, rk + (size_t)n * dk, ru + (size_t)n * dv);
             if (++n == W) {
@@ -662,8 +693,9 @@ int OQ(run_baseline)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
         for (int i = 0; i < dk * dv; ++i) S[i] = state_round(mode, (real)S_init[(size_t)t * dk * dv + i]);
         for (int s = 0; s < T; ++s) {
             const size_t ts = (size_t)t * T + s;
-            recurrent_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, in->v + ts * dv,
-                                in->alpha + ts * g, in->beta[ts], o ? o + ts * dv : od, mode, w);
+            recurrent_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, read_vec(in, ts, dk),
+                                in->v + ts * dv, in->alpha + ts * g, in->beta[ts], o ? o + ts * dv : od,
+                                mode, w);
         }
         if (S_final)
             for (int i = 0; i < dk * dv; ++i) S_final[(size_t)t * dk * dv + i] = (double)S[i];
@@ -709,10 +741,10 @@ int OQ(run_drift)(const lqo_cfg *cfg, int tiles, int T, int every, const double 
         int n = 0;
         for (int s = 0; s < T; ++s) {
             const size_t ts = (size_t)t * T + s;
-            window_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, in->v + ts * dv,
-                             in->alpha + ts * g, in->beta[ts], o1, ra, rk, ru, u);
-            recurrent_step_impl(cfg, F, in->q + ts * dk, in->k + ts * dk, in->v + ts * dv,
-                                in->alpha + ts * g, in->beta[ts], o2, LQO_STATE_F32, u);
+            window_step_impl(cfg, S, in->q + ts * dk, in->k + ts * dk, read_vec(in, ts, dk),
+                             in->v + ts * dv, in->alpha + ts * g, in->beta[ts], o1, ra, rk, ru, u);
+            recurrent_step_impl(cfg, F, in->q + ts * dk, in->k + ts * dk, read_vec(in, ts, dk),
+                                in->v + ts * dv, in->alpha + ts * g, in->beta[ts], o2, LQO_STATE_F32, u);
             if (++n == W) {
                 for (int i = 0; i < dk * dv; ++i) Sd[i] = (double)S[i];
                 quantize_impl(cfg, Sd, Z, delta, c, Kt, Ut);

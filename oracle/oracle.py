@@ -40,7 +40,7 @@ class Cfg(C.Structure):
 
 
 class _Inputs(C.Structure):
-    _fields_ = [(n, C.c_void_p) for n in ("q", "k", "v", "alpha", "beta")]
+    _fields_ = [(n, C.c_void_p) for n in ("q", "k", "v", "alpha", "beta", "b")]
 
 
 class _Outputs(C.Structure):
@@ -50,7 +50,7 @@ class _Outputs(C.Structure):
 
 
 GATE_SCALAR, GATE_DIAG = 0, 1
-RULE_DELTA, RULE_ADD = 0, 1    # b_t = D_t k_t (delta rule) or b_t = 0
+RULE_DELTA, RULE_ADD, RULE_GENERAL = 0, 1, 2   # b_t = D_t k_t (delta rule), b_t = 0, b_t given
 CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6 = 0, 1, 2, 3
 STATE_EXACT, STATE_F32, STATE_BF16 = 0, 1, 2
 
@@ -69,9 +69,9 @@ def _declare(L):
     for pre in ("lqo64_", "lqo32_"):
         getattr(L, pre + "quantize").argtypes = [vp] * 7
         getattr(L, pre + "dequantize").argtypes = [vp] * 7
-        getattr(L, pre + "recurrent_step").argtypes = [vp, vp, vp, vp, vp, vp, f32, vp, i32]
-        getattr(L, pre + "window_step").argtypes = [vp, vp, vp, vp, vp, vp, f32, vp, vp, vp, vp]
-        getattr(L, pre + "readout_step").argtypes = [vp] * 10 + [i32] + [vp] * 4 + [f32] + [vp] * 4
+        getattr(L, pre + "recurrent_step").argtypes = [vp, vp, vp, vp, vp, vp, vp, f32, vp, i32]
+        getattr(L, pre + "window_step").argtypes = [vp, vp, vp, vp, vp, vp, vp, f32, vp, vp, vp, vp]
+        getattr(L, pre + "readout_step").argtypes = [vp] * 10 + [i32] + [vp] * 5 + [f32] + [vp] * 4
         getattr(L, pre + "reconstruct").argtypes = [vp] * 10 + [i32, vp]
         for fn in ("run_dense", "run_readout"):
             getattr(L, pre + fn).argtypes = [vp, i32, i32, vp, vp, vp, vp, i32]
@@ -163,27 +163,42 @@ def _f32(a):
     return np.ascontiguousarray(a, dtype=np.float32)
 
 
-def recurrent_step(cfg: Cfg, S, q, k, v, alpha, beta, mode=STATE_EXACT, prec=64):
+def _read_vec(cfg: Cfg, b):
+    """The read vector argument: required by the general rule, unused otherwise."""
+    if cfg.rule == RULE_GENERAL:
+        if b is None:
+            raise ValueError("the general rule needs the read vector b")
+        b = _f32(b)
+        if b.shape != (cfg.dk,):
+            raise ValueError(f"b must have shape ({cfg.dk},)")
+        return b
+    return None
+
+
+def recurrent_step(cfg: Cfg, S, q, k, v, alpha, beta, mode=STATE_EXACT, prec=64, b=None):
     """One token of the unquantized recurrence; returns (S_new, o)."""
     S = np.array(S, dtype=np.float64, order="C")
     o = np.zeros(cfg.dv)
     alpha = _f32(np.atleast_1d(alpha))
-    _fn("recurrent_step", prec)(C.byref(cfg), _p(S), _p(_f32(q)), _p(_f32(k)), _p(_f32(v)),
+    bv = _read_vec(cfg, b)
+    _fn("recurrent_step", prec)(C.byref(cfg), _p(S), _p(_f32(q)), _p(_f32(k)), _p(bv), _p(_f32(v)),
                                 _p(alpha), float(beta), _p(o), mode)
     return S, o
 
 
-def window_step(cfg: Cfg, S, q, k, v, alpha, beta, prec=64):
+def window_step(cfg: Cfg, S, q, k, v, alpha, beta, prec=64, b=None):
     """One token of the per-window method, dense form; returns (S_new, o, (a, k~, u))."""
     S = np.array(S, dtype=np.float64, order="C")
     g = cfg.dk if cfg.gate else 1
     o, ra, rk, ru = np.zeros(cfg.dv), np.zeros(g), np.zeros(cfg.dk), np.zeros(cfg.dv)
-    _fn("window_step", prec)(C.byref(cfg), _p(S), _p(_f32(q)), _p(_f32(k)), _p(_f32(v)),
+    bv = _read_vec(cfg, b)
+    _fn("window_step", prec)(C.byref(cfg), _p(S), _p(_f32(q)), _p(_f32(k)), _p(bv), _p(_f32(v)),
                              _p(_f32(np.atleast_1d(alpha))), float(beta), _p(o), _p(ra), _p(rk), _p(ru))
     return S, o, (ra, rk, ru)
 
 
-def readout_step(cfg: Cfg, rep: Rep | None, S0, rec_a, rec_k, rec_u, q, k, v, alpha, beta, prec=64):
+def readout_step(cfg: Cfg, rep: Rep | None, S0, rec_a, rec_k, rec_u, q, k, v, alpha, beta, prec=64,
+                 b=None):
     """One token in readout form from a fixed base; returns (o, (a, k~, u))."""
     g = cfg.dk if cfg.gate else 1
     n = 0 if rec_a is None else len(rec_a)
@@ -197,8 +212,9 @@ def readout_step(cfg: Cfg, rep: Rep | None, S0, rec_a, rec_k, rec_u, q, k, v, al
         Kt = np.ascontiguousarray(rep.Kt) if cfg.n_comp else np.zeros((1, cfg.dk))
         Ut = np.ascontiguousarray(rep.Ut) if cfg.n_comp else np.zeros((1, cfg.dv))
         args = [_p(np.ascontiguousarray(rep.Z)), _p(rep.delta), _p(rep.c), _p(Kt), _p(Ut), None]
+    bv = _read_vec(cfg, b)
     _fn("readout_step", prec)(C.byref(cfg), *args, _p(ra), _p(rk), _p(ru), n, _p(_f32(q)),
-                              _p(_f32(k)), _p(_f32(v)), _p(_f32(np.atleast_1d(alpha))),
+                              _p(_f32(k)), _p(bv), _p(_f32(v)), _p(_f32(np.atleast_1d(alpha))),
                               float(beta), _p(o), _p(na), _p(nk), _p(nu))
     return o, (na, nk, nu)
 
@@ -234,7 +250,11 @@ def _inputs(tok: dict, tiles: int, T: int, cfg: Cfg):
         "alpha": _f32(tok["alpha"]).reshape(tiles, T, g),
         "beta": _f32(tok["beta"]).reshape(tiles, T),
     }
-    st = _Inputs(*[_p(arrs[n]) for n in ("q", "k", "v", "alpha", "beta")])
+    if cfg.rule == RULE_GENERAL:
+        if "b" not in tok:
+            raise ValueError("the general rule needs read vectors tok['b'] [tiles][T][dk]")
+        arrs["b"] = _f32(tok["b"]).reshape(tiles, T, cfg.dk)
+    st = _Inputs(*[_p(arrs.get(n)) for n in ("q", "k", "v", "alpha", "beta", "b")])
     return st, arrs
 
 

@@ -1,7 +1,9 @@
 """Pins of the CPU oracle against what the paper and the mathematics fix.
 
 Recurrence (Sec. 3.1 Eq. (general), App. A): the native GDN / KDA updates, the
-delta-rule write, degenerate gates.  Quantizer (Secs. 3.3-3.4, App. B.3):
+additive rows, the general read-vector rule and the split-token instances
+(RWKV7 as erase + write, DeltaProduct as n Householder sub-steps) against
+explicit matrix forms, the delta-rule write, degenerate gates.  Quantizer (Secs. 3.3-3.4, App. B.3):
 exhaustive code search, error bounds, scaling / sign / permutation symmetry,
 Eckart-Young optimality of the fitted tokens.  Window method (Sec. 3.2,
 App. B.1-B.3): unrolling equals the recurrence, W=1 without tokens is the naive
@@ -79,6 +81,136 @@ def test_additive_instances_native_forms(O, gate):
         S, _ = O.recurrent_step(cl, S, q, k, v, f32([1.0]), 1.0)
         acc += np.outer(k.astype(np.float64), v.astype(np.float64))
     assert rel(S, acc) < 1e-14
+
+
+@pytest.mark.parametrize("gate", [0, 1])
+def test_general_rule_special_cases(O, gate):
+    """General rule (read vector given): b = D_t k reproduces the delta rule (up
+    to the fp32 rounding of the product a k), b = 0 the additive rule exactly,
+    in the recurrence, the dense window step and the readout form from a
+    quantized base (exact records, so that no FP16 rounding of a correction can
+    flip on that last-bit difference)."""
+    rng = np.random.default_rng(17 + gate)
+    dk, dv = 16, 12
+    cg, cd, ca = (O.make_cfg(dk=dk, dv=dv, gate=gate, n_comp=2, window=8, round_records=0, rule=r)
+                  for r in (O.RULE_GENERAL, O.RULE_DELTA, O.RULE_ADD))
+    S = _state(rng, dk, dv)
+    rep = O.quantize(cg, S)
+    ra, rk, ru = [], [], []
+    for _ in range(4):
+        q, k, v = unit(rng, dk), unit(rng, dk), f32(rng.standard_normal(dv))
+        beta = np.float32(rng.uniform(0.1, 0.9))
+        a = f32(rng.uniform(0.5, 1.0, dk if gate else 1))
+        bk = f32(a * k)
+        z = np.zeros(dk, np.float32)
+        for fn in (O.recurrent_step, O.window_step):
+            g1, g0 = fn(cg, S, q, k, v, a, beta, b=bk), fn(cd, S, q, k, v, a, beta)
+            assert rel(g1[0], g0[0]) < 1e-6 and rel(g1[1], g0[1]) < 1e-6
+            z1, z0 = fn(cg, S, q, k, v, a, beta, b=z), fn(ca, S, q, k, v, a, beta)
+            assert np.array_equal(z1[0], z0[0]) and np.array_equal(z1[1], z0[1])
+        recs = (np.array(ra), np.array(rk), np.array(ru)) if ra else (None, None, None)
+        o1, n1 = O.readout_step(cg, rep, None, *recs, q, k, v, a, beta, b=bk)
+        o0, n0 = O.readout_step(cd, rep, None, *recs, q, k, v, a, beta)
+        assert rel(o1, o0) < 1e-6 and rel(n1[2], n0[2]) < 1e-6
+        oz, nz = O.readout_step(cg, rep, None, *recs, q, k, v, a, beta, b=z)
+        oa, na = O.readout_step(ca, rep, None, *recs, q, k, v, a, beta)
+        assert np.array_equal(oz, oa) and np.array_equal(nz[2], na[2])
+        ra.append(n0[0]), rk.append(n0[1]), ru.append(n0[2])
+        S = O.window_step(cd, S, q, k, v, a, beta)[0]
+
+
+def test_rwkv7_two_substeps_native_transition(O):
+    """RWKV7 (App. A): the erase sub-step (general rule, b = a.kappa, v = 0)
+    followed by the pure write (b = 0, D = I) is one token of the native
+    transition S_t = (Diag(w) - kappa (a.kappa)^T) S_{t-1} + k v^T, o_t = S_t^T r,
+    written here as explicit d_k x d_k matrices.  Checked on the recurrence and
+    on both forms of the per-window method (quantization off, exact records),
+    with windows that end between the two sub-steps of a token."""
+    from tests import instances
+    rng = np.random.default_rng(18)
+    dk, dv, tiles, T = 16, 12, 2, 11
+    raw = instances.rwkv7_raw(rng, tiles, T, dk, dv)
+    tok = instances.rwkv7_substeps(raw)
+    S0 = rng.standard_normal((tiles, dk, dv))
+    o_nat = np.zeros((tiles, T, dv))
+    S_nat = S0.copy()
+    for i in range(tiles):
+        S = S0[i]
+        for t in range(T):
+            w, a, kap, k, r, v = (raw[n][i, t].astype(np.float64) for n in ("w", "a", "kappa", "k", "r", "v"))
+            bvec = f32(raw["a"][i, t] * raw["kappa"][i, t]).astype(np.float64)
+            assert np.allclose(bvec, a * kap, rtol=1e-7)
+            S = (np.diag(w) - np.outer(kap, bvec)) @ S + np.outer(k, v)
+            o_nat[i, t] = S.T @ r
+        S_nat[i] = S
+    cfg_b = O.make_cfg(dk=dk, dv=dv, gate=1, rule=O.RULE_GENERAL)
+    o_ref, S_ref = O.run_baseline(cfg_b, S0, tok, mode=O.STATE_EXACT)
+    assert rel(o_ref[:, 1::2], o_nat) < 1e-13
+    assert rel(S_ref, S_nat) < 1e-13
+    for W in (5, 8):
+        cfg = O.make_cfg(dk=dk, dv=dv, window=W, n_comp=2, gate=1, quantize=0, round_records=0,
+                         rule=O.RULE_GENERAL)
+        for run in (O.run_dense, O.run_readout):
+            res = run(cfg, S0, tok, snapshots=False)
+            assert rel(res["o"][:, 1::2], o_nat) < 1e-12
+            assert rel(res["S_final"], S_nat) < 1e-12
+    # the pin separates the plausible misreading that reads b against the decayed
+    # state, (D S)^T b, from the paper's S^T b
+    Sw = S0[0]
+    for t in range(T):
+        w, kap, k, v = (raw[n][0, t].astype(np.float64) for n in ("w", "kappa", "k", "v"))
+        bvec = f32(raw["a"][0, t] * raw["kappa"][0, t]).astype(np.float64)
+        A = np.diag(w) @ Sw
+        Sw = A - np.outer(kap, A.T @ bvec) + np.outer(k, v)
+    assert rel(Sw, S_nat[0]) > 1e-3
+
+
+def test_deltaproduct_substeps_native_householder_product(O):
+    """DeltaProduct (App. A), n = 3 delta-rule sub-steps per token with the
+    token's scalar gate on the first: S_t = a_t P_n..P_1 S_{t-1} + sum_j
+    P_n..P_{j+1} beta_j k_j v_j^T with P_j = I - beta_j k_j k_j^T, as explicit
+    matrix products.  Recurrence and both window forms."""
+    from tests import instances
+    rng = np.random.default_rng(19)
+    dk, dv, tiles, T, n = 16, 12, 2, 7, 3
+    q = rng.standard_normal((tiles, T * n, dk))
+    k = rng.standard_normal((tiles, T * n, dk))
+    sub = {"q": f32(q / np.linalg.norm(q, axis=-1, keepdims=True)),
+           "k": f32(k / np.linalg.norm(k, axis=-1, keepdims=True)),
+           "v": f32(rng.standard_normal((tiles, T * n, dv))),
+           "beta": f32(rng.uniform(0.0, 2.0, (tiles, T * n))),      # negative eigenvalues allowed
+           "alpha": f32(rng.uniform(0.6, 1.0, (tiles, T, 1)))}
+    tok = instances.deltaproduct_substeps(sub, n)
+    S0 = rng.standard_normal((tiles, dk, dv))
+    o_nat, S_nat = np.zeros((tiles, T, dv)), S0.copy()
+    for i in range(tiles):
+        S = S0[i]
+        for t in range(T):
+            js = range(t * n, (t + 1) * n)
+            Ps = [np.eye(dk) - np.float64(sub["beta"][i, j]) *
+                  np.outer(sub["k"][i, j].astype(np.float64), sub["k"][i, j].astype(np.float64)) for j in js]
+            prod = np.eye(dk)
+            for P in Ps:
+                prod = P @ prod
+            Snew = np.float64(sub["alpha"][i, t, 0]) * prod @ S
+            for m, j in enumerate(js):
+                tail = np.eye(dk)
+                for P in Ps[m + 1:]:
+                    tail = P @ tail
+                Snew += tail @ (np.float64(sub["beta"][i, j]) * np.outer(sub["k"][i, j].astype(np.float64),
+                                                                          sub["v"][i, j].astype(np.float64)))
+            S = Snew
+            o_nat[i, t] = S.T @ sub["q"][i, t * n + n - 1].astype(np.float64)
+        S_nat[i] = S
+    cfg_b = O.make_cfg(dk=dk, dv=dv, gate=0)
+    o_ref, S_ref = O.run_baseline(cfg_b, S0, tok, mode=O.STATE_EXACT)
+    assert rel(o_ref[:, n - 1::n], o_nat) < 1e-12
+    assert rel(S_ref, S_nat) < 1e-12
+    cfg = O.make_cfg(dk=dk, dv=dv, window=4, n_comp=2, gate=0, quantize=0, round_records=0)
+    for run in (O.run_dense, O.run_readout):
+        res = run(cfg, S0, tok, snapshots=False)
+        assert rel(res["o"][:, n - 1::n], o_nat) < 1e-12
+        assert rel(res["S_final"], S_nat) < 1e-12
 
 
 def test_delta_rule_writes_value_exactly(O):
@@ -371,6 +503,28 @@ def test_readout_form_equals_dense_form(O, gate, code, r, smooth):
     assert np.mean(b["Z"] == d["Z"]) > 0.9999
     assert rel(b["S_final"], d["S_final"]) < 1e-10
     assert np.array_equal(b["rec_len"], d["rec_len"])
+    n = int(d["rec_len"][0])
+    assert rel(b["rec_u"][:, :n], d["rec_u"][:, :n]) < 1e-12
+
+
+@pytest.mark.parametrize("gate", [0, 1])
+def test_readout_form_equals_dense_form_general_rule(O, gate):
+    """The same agreement under the general rule: RWKV7 sub-steps (per-channel
+    gate) and, for the scalar gate, read vectors drawn independently of the key."""
+    from tests import instances
+    rng = np.random.default_rng(75 + gate)
+    dk = dv = 64
+    S0 = _state(rng, dk, dv)[None].repeat(2, 0) * rng.uniform(0.5, 2, (2, 1, 1))
+    if gate:
+        tok = instances.rwkv7_substeps(instances.rwkv7_raw(rng, 2, 23, dk, dv))
+    else:
+        tok = _tokens(rng, 2, 46, dk, dv, 0)
+        tok["b"] = f32(0.8 * rng.standard_normal((2, 46, dk)) / np.sqrt(dk))
+    cfg = O.make_cfg(dk=dk, dv=dv, window=16, n_comp=4, gate=gate, rule=O.RULE_GENERAL)
+    d, b = O.run_dense(cfg, S0, tok), O.run_readout(cfg, S0, tok)
+    assert rel(b["o"], d["o"]) < 1e-10
+    assert np.mean(b["Z"] == d["Z"]) > 0.9999
+    assert rel(b["S_final"], d["S_final"]) < 1e-10
     n = int(d["rec_len"][0])
     assert rel(b["rec_u"][:, :n], d["rec_u"][:, :n]) < 1e-12
 
