@@ -221,17 +221,20 @@ def per_launch_times(wl, dims, S0, toks, reps=3):
     """Average kernel durations, measured with HIP events on the stream the
     kernels run on: the decode launches of one whole window (positions 1..W)
     replayed as one graph, divided by W; the commit that ends the window; the
-    window-start quantization."""
+    window-start quantization.  toks = (q, k, v, alpha, beta), or (q, k, b, v,
+    alpha, beta) for the general rule (read vectors b given)."""
     import torch
     from paper_2609_38166_amd import binding as B_
     st = B_.State.empty(dims)
     o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
-    q, k, v, a, b = toks
     W = wl.window
 
     def window():
         for i in range(W):
-            B_.leapquant_decode_step(dims, st, q[i], k[i], v[i], a[i], b[i], o)
+            if len(toks) == 6:
+                B_.leapquant_decode_step_general(dims, st, *(t_[i] for t_ in toks), o)
+            else:
+                B_.leapquant_decode_step(dims, st, *(t_[i] for t_ in toks), o)
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -272,6 +275,41 @@ def per_launch_times(wl, dims, S0, toks, reps=3):
     return {k_: float(np.mean(v_)) for k_, v_ in (("decode_ms", res["decode"]),
                                                    ("commit_ms", res["commit"]),
                                                    ("quantize_ms", res["quantize"]))}
+
+
+def rwkv7_tokens(wl, n_sub, seed):
+    """Step-major device inputs of n_sub / 2 RWKV7 tokens as general-rule
+    sub-steps (q, k, b, v, alpha, beta): an erase with alpha = w, k = kappa,
+    b = a . kappa, v = 0, then a write with alpha = 1, k = k, b = 0, v = v; both
+    take the receptance r as query and beta = 1.  Drawn on the device:
+    w = exp(-e^-0.5 sigmoid(z)), a = sigmoid(z), kappa, k, r unit-norm
+    Gaussian, v ~ N(0, I)."""
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    n = n_sub // 2
+    shp = (n, wl.batch, wl.heads_v, wl.dk)
+
+    def rnd(shape=shp):
+        return torch.randn(shape, generator=g, device="cuda")
+
+    def unit():
+        x = rnd()
+        return x / x.norm(dim=-1, keepdim=True)
+
+    def inter(x0, x1):
+        out = torch.empty((2 * n,) + tuple(x0.shape[1:]), device="cuda")
+        out[0::2], out[1::2] = x0, x1
+        return out
+
+    w = torch.exp(-np.exp(-0.5) * torch.sigmoid(rnd()))
+    a = torch.sigmoid(rnd())
+    kap, k, r = unit(), unit(), unit()
+    v = rnd((n, wl.batch, wl.heads_v, wl.dv))
+    zero = torch.zeros(shp, device="cuda")
+    toks = (inter(r, r), inter(kap, k), inter(a * kap, zero), inter(torch.zeros_like(v), v),
+            inter(w, torch.ones(shp, device="cuda")), torch.ones((2 * n, wl.batch, wl.heads_v), device="cuda"))
+    return tuple(t_.contiguous() for t_ in toks)
 
 
 def decode_two_batches(wl, dims, S0, toks, reps=3):
@@ -598,6 +636,28 @@ def main():
                           "decode_gbps": round(vb / (vk["decode_ms"] * 1e-3) / 1e9, 1)}
             log(f"[bench] {vname}: {var[vname]}")
         out["code_variants"] = var
+
+        # RWKV7 at the same shape (App. A): two general-rule sub-steps per token,
+        # W = 64 sub-steps (32 tokens) per window, per-channel gate, r = 8, int8
+        rw = wl.with_(name="rwkv7_kimi_shape", rule=2)
+        rd = B_.make_dims(rw.batch, rw.heads_v, rw.heads_v, window=rw.window, n_comp=rw.n_comp,
+                          power_iters=rw.power_iters, gate=rw.gate, code=rw.code, rule=2)
+        r_toks = rwkv7_tokens(rw, rw.window, 20260010)
+        rk_ = per_launch_times(rw, rd, S0, r_toks)
+        n_sub = 2 * rw.steps
+        rstep = (rk_["decode_ms"] * n_sub + rk_["commit_ms"] * (n_sub // rw.window) + rk_["quantize_ms"])
+        rb = float(np.mean([decode_bytes(rw, i) for i in range(1, rw.window + 1)])) * rw.tiles
+        # per sub-step: q, k, b, v, alpha, beta inputs (the general rule reads b as well)
+        rb += 4 * rw.dk * rw.tiles
+        out["rwkv7"] = {"tiles": rw.tiles, "tokens": rw.steps, "sub_steps_per_window": rw.window,
+                        "value": round(rw.tiles * rw.steps / (rstep * 1e-3), 1),
+                        "unit": "token-head steps/s (two decode launches per token)",
+                        "ms_per_step_from_kernels": round(rstep, 3),
+                        "decode_us": round(rk_["decode_ms"] * 1e3, 2),
+                        "decode_gbps": round(rb / (rk_["decode_ms"] * 1e-3) / 1e9, 1),
+                        "commit_us": round(rk_["commit_ms"] * 1e3, 2)}
+        log(f"[bench] rwkv7: {out['rwkv7']}")
+        del r_toks
 
     if not args.no_baselines:
         q, k, v, a, b = toks

@@ -59,6 +59,8 @@ extern "C" {
 #define LQ_RULE_DELTA  0     /* delta rule: b_t = D_t k_t (DeltaNet, GDN, KDA)        */
 #define LQ_RULE_ADD    1     /* b_t = 0: u_t = v_t (linear attention, RetNet, Mamba2,
                               * GLA / RWKV6 / HGRN2 with the matching gate)           */
+#define LQ_RULE_GENERAL 2    /* b_t given with every token (App. A general form): the
+                              * erase sub-step of RWKV7; only the *_general calls    */
 #define LQ_STATE_F32   0     /* baseline state in fp32                               */
 #define LQ_STATE_BF16  1     /* baseline state in bf16, rounded to nearest even      */
 
@@ -86,8 +88,11 @@ typedef struct {
     int32_t gate;        /* LQ_GATE_SCALAR or LQ_GATE_DIAG                            */
     int32_t code;        /* LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4 or LQ_CODE_INT6  */
     int32_t smooth;      /* 1: residual smoothing (Sec. 3.4); 0: c = 1               */
-    int32_t rule;        /* LQ_RULE_DELTA or LQ_RULE_ADD: the read vector b_t of the
-                          * general recurrence (App. A instance table)               */
+    int32_t rule;        /* LQ_RULE_DELTA, LQ_RULE_ADD or LQ_RULE_GENERAL: the read
+                          * vector b_t of the general recurrence (App. A table).
+                          * Only the decode and baseline steps read it; the state
+                          * layout does not depend on it, so one state may be
+                          * stepped under different rules (see the general step) */
 } lq_dims;
 
 /* The quantized state of all tiles (device pointers, caller-owned).
@@ -149,11 +154,38 @@ int32_t leapquant_quantize_state(const lq_dims *dims, const float *S, lq_state *
  *   u_i = fp16(v - A^T k),  k~_i = fp16(beta k),  o = A^T q + u_i (k~_i . q)
  * and the record (alpha_i, k~_i, u_i) is appended; rec_len += 1.  A tile whose
  * rec_len already equals W is not modified: its o is NaN and
- * LQ_DEVERR_WINDOW_FULL is raised in *err.
+ * LQ_DEVERR_WINDOW_FULL is raised in *err.  dims->rule LQ_RULE_GENERAL is
+ * rejected (LQ_EINVAL): that rule takes its read vectors through
+ * leapquant_decode_step_general.
  */
 int32_t leapquant_decode_step(const lq_dims *dims, lq_state *st, const float *q, const float *k,
                               const float *v, const float *alpha, const float *beta, float *o,
                               void *stream);
+
+/*
+ * leapquant_decode_step_general -- one token for every tile under the general
+ * recurrence with the read vector given (App. A, Eq. (general)):
+ *   S_t = D_t S_{t-1} + (beta_t k_t) (v_t - S_{t-1}^T b_t)^T,  o_t = S_t^T q_t.
+ *   b      [B][heads_v][d_k] fp32, the read vectors (one per tile);
+ *          other arguments as leapquant_decode_step.
+ * dims->rule must be LQ_RULE_GENERAL (LQ_EINVAL otherwise; leapquant_decode_step
+ * rejects that rule).  With i = rec_len + 1 and d_i the token's FP16 decay,
+ *   S_{i-1}^T b = delta . (Z^T (c . Gamma_{1:i-1} b)) + U~ (K~^T Gamma_{1:i-1} b)
+ *                 + sum_{j<i} u_j (k~_j^T Gamma_{j+1:i-1} b),
+ * and A^T q = S_{i-1}^T (d_i . q) by the same sum; then u_i = fp16(v - S_{i-1}^T b),
+ * o = A^T q + u_i (k~_i . q) and the record is appended as in
+ * leapquant_decode_step.  A model whose erase direction differs from its write
+ * key runs as sub-steps (App. A): an RWKV7 token with transition
+ * Diag(w) - kappa (a . kappa)^T and write k v^T is this call with alpha = w,
+ * k = kappa, beta = 1, b = a . kappa, v = 0 (diagonal gate), then either this
+ * call with alpha = 1, b = 0, or leapquant_decode_step on the same state with a
+ * copy of dims whose rule is LQ_RULE_ADD, with k = k, beta = 1, v = v; each
+ * sub-step is one record, so W counts sub-steps.
+ */
+int32_t leapquant_decode_step_general(const lq_dims *dims, lq_state *st, const float *q,
+                                      const float *k, const float *b, const float *v,
+                                      const float *alpha, const float *beta, float *o,
+                                      void *stream);
 
 /*
  * leapquant_window_commit -- end the window of the selected tiles.  Sec. 3.3
@@ -177,11 +209,22 @@ int32_t leapquant_window_commit(const lq_dims *dims, lq_state *st, const int32_t
  * state S [B][heads_v][d_v][d_k] updated in place, fp32 (LQ_STATE_F32) or
  * bf16 bits (LQ_STATE_BF16, rounded to nearest even after the step).
  * Arithmetic is fp32.  Other arguments as leapquant_decode_step (the decay is
- * not rounded).
+ * not rounded); LQ_RULE_GENERAL is rejected as there.
  */
 int32_t leapquant_baseline_step(const lq_dims *dims, void *S, int32_t state_dtype,
                                 const float *q, const float *k, const float *v,
                                 const float *alpha, const float *beta, float *o, void *stream);
+
+/*
+ * leapquant_baseline_step_general -- leapquant_baseline_step under the general
+ * recurrence (App. A, Eq. (general)) with the read vectors b [B][heads_v][d_k]
+ * fp32:  u = v - S^T b,  S = D S + (beta k) u^T,  o = S^T q.
+ * dims->rule must be LQ_RULE_GENERAL (LQ_EINVAL otherwise).
+ */
+int32_t leapquant_baseline_step_general(const lq_dims *dims, void *S, int32_t state_dtype,
+                                        const float *q, const float *k, const float *b,
+                                        const float *v, const float *alpha, const float *beta,
+                                        float *o, void *stream);
 
 /*
  * leapquant_dequantize_state -- materialise the current fp32 state of every

@@ -20,12 +20,13 @@ LQ_GATE_SCALAR, LQ_GATE_DIAG = 0, 1
 LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4, LQ_CODE_INT6 = 0, 1, 2, 3
 CODE_BITS = {LQ_CODE_INT8: 8, LQ_CODE_E4M3: 8, LQ_CODE_INT4: 4, LQ_CODE_INT6: 6}
 LQ_STATE_F32, LQ_STATE_BF16 = 0, 1
-LQ_RULE_DELTA, LQ_RULE_ADD = 0, 1
+LQ_RULE_DELTA, LQ_RULE_ADD, LQ_RULE_GENERAL = 0, 1, 2
 LQ_DEVERR_WINDOW_FULL = 1
 LQ_DEVERR_BAD_REC_LEN = 2
 
 EXPORTS = ("leapquant_state_bytes", "leapquant_quantize_state", "leapquant_decode_step",
-           "leapquant_window_commit", "leapquant_baseline_step", "leapquant_dequantize_state",
+           "leapquant_decode_step_general", "leapquant_window_commit", "leapquant_baseline_step",
+           "leapquant_baseline_step_general", "leapquant_dequantize_state",
            "leapquant_check_error", "leapquant_strerror", "leapquant_last_hip_error")
 
 
@@ -63,8 +64,10 @@ def _lib():
         L.leapquant_state_bytes.argtypes = [vp, vp]
         L.leapquant_quantize_state.argtypes = [vp, vp, vp, vp]
         L.leapquant_decode_step.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.leapquant_decode_step_general.argtypes = [vp] * 10
         L.leapquant_window_commit.argtypes = [vp, vp, vp, vp]
         L.leapquant_baseline_step.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.leapquant_baseline_step_general.argtypes = [vp, vp, i32] + [vp] * 8
         L.leapquant_dequantize_state.argtypes = [vp, vp, vp, vp]
         L.leapquant_check_error.argtypes = [vp, vp, vp]
         L.leapquant_strerror.argtypes = [i32]
@@ -130,6 +133,10 @@ def _check_tokens(dims, q, k, v, alpha, beta, o):
     _need(alpha, t * g * 4, "alpha")
     _need(beta, t * 4, "beta")
     _need(o, t * dims.d_v * 4, "o")
+
+
+def _check_read(dims, b):
+    _need(b, dims.batch * dims.heads_v * dims.d_k * 4, "b")
 
 
 def _stream(stream):
@@ -216,6 +223,20 @@ def leapquant_decode_step(dims: lq_dims, st: State, q, k, v, alpha, beta, o, str
            "leapquant_decode_step")
 
 
+def leapquant_decode_step_general(dims: lq_dims, st: State, q, k, b, v, alpha, beta, o,
+                                  stream=None):
+    """Decode step with the read vectors b [B][heads_v][d_k] given (dims.rule
+    must be LQ_RULE_GENERAL)."""
+    _check_state(dims, st)
+    _check_tokens(dims, q, k, v, alpha, beta, o)
+    _check_read(dims, b)
+    s = st.struct()
+    _check(_lib().leapquant_decode_step_general(C.byref(dims), C.byref(s), _ptr(q), _ptr(k), _ptr(b),
+                                                _ptr(v), _ptr(alpha), _ptr(beta), _ptr(o),
+                                                _stream(stream)),
+           "leapquant_decode_step_general")
+
+
 def leapquant_window_commit(dims: lq_dims, st: State, mask=None, stream=None):
     _check_state(dims, st)
     if mask is not None:
@@ -234,6 +255,18 @@ def leapquant_baseline_step(dims: lq_dims, S, state_dtype: int, q, k, v, alpha, 
                                           _ptr(v), _ptr(alpha), _ptr(beta), _ptr(o),
                                           _stream(stream)),
            "leapquant_baseline_step")
+
+
+def leapquant_baseline_step_general(dims: lq_dims, S, state_dtype: int, q, k, b, v, alpha, beta, o,
+                                    stream=None):
+    width = 2 if state_dtype == LQ_STATE_BF16 else 4
+    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * width, "S")
+    _check_tokens(dims, q, k, v, alpha, beta, o)
+    _check_read(dims, b)
+    _check(_lib().leapquant_baseline_step_general(C.byref(dims), _ptr(S), state_dtype, _ptr(q),
+                                                  _ptr(k), _ptr(b), _ptr(v), _ptr(alpha), _ptr(beta),
+                                                  _ptr(o), _stream(stream)),
+           "leapquant_baseline_step_general")
 
 
 def leapquant_dequantize_state(dims: lq_dims, st: State, S_out, stream=None):

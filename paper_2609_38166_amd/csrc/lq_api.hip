@@ -38,7 +38,8 @@ int32_t check_dims(const lq_dims *d) {
         d->code != LQ_CODE_INT6)
         return LQ_EINVAL;
     if (d->smooth != 0 && d->smooth != 1) return LQ_EINVAL;
-    if (d->rule != LQ_RULE_DELTA && d->rule != LQ_RULE_ADD) return LQ_EINVAL;
+    if (d->rule != LQ_RULE_DELTA && d->rule != LQ_RULE_ADD && d->rule != LQ_RULE_GENERAL)
+        return LQ_EINVAL;
     if (d->d_k != 128 || d->d_v != 128) return LQ_EUNSUPPORTED;
     if (d->n_comp > LQ_MAX_COMP) return LQ_EUNSUPPORTED;
     if (d->n_comp > 0 && (d->power_iters < 1 || d->power_iters > LQ_MAX_POWER_ITERS))
@@ -132,8 +133,23 @@ int32_t leapquant_decode_step(const lq_dims *d, lq_state *st, const float *q, co
     int32_t e = check_dims(d);
     if (e != LQ_OK) return e;
     if ((e = check_state(d, st)) != LQ_OK) return e;
+    if (d->rule == LQ_RULE_GENERAL) return LQ_EINVAL;   // needs the read vectors
     if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
-    lq::TokenPtrs t{q, k, v, alpha, beta, o};
+    lq::TokenPtrs t{q, k, v, alpha, beta, o, nullptr};
+    return hip_status(lq::launch_decode(*d, state_ptrs(st), t, (hipStream_t)stream));
+}
+
+int32_t leapquant_decode_step_general(const lq_dims *d, lq_state *st, const float *q,
+                                      const float *k, const float *b, const float *v,
+                                      const float *alpha, const float *beta, float *o,
+                                      void *stream) {
+    int32_t e = check_dims(d);
+    if (e != LQ_OK) return e;
+    if ((e = check_state(d, st)) != LQ_OK) return e;
+    if (d->rule != LQ_RULE_GENERAL) return LQ_EINVAL;
+    if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    if ((e = check_ptr(b)) != LQ_OK) return e;
+    lq::TokenPtrs t{q, k, v, alpha, beta, o, b};
     return hip_status(lq::launch_decode(*d, state_ptrs(st), t, (hipStream_t)stream));
 }
 
@@ -153,8 +169,24 @@ int32_t leapquant_baseline_step(const lq_dims *d, void *S, int32_t state_dtype, 
     if (e != LQ_OK) return e;
     if (state_dtype != LQ_STATE_F32 && state_dtype != LQ_STATE_BF16) return LQ_EINVAL;
     if ((e = check_ptr(S)) != LQ_OK) return e;
+    if (d->rule == LQ_RULE_GENERAL) return LQ_EINVAL;   // needs the read vectors
     if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
-    lq::TokenPtrs t{q, k, v, alpha, beta, o};
+    lq::TokenPtrs t{q, k, v, alpha, beta, o, nullptr};
+    return hip_status(lq::launch_baseline(*d, S, state_dtype, t, (hipStream_t)stream));
+}
+
+int32_t leapquant_baseline_step_general(const lq_dims *d, void *S, int32_t state_dtype,
+                                        const float *q, const float *k, const float *b,
+                                        const float *v, const float *alpha, const float *beta,
+                                        float *o, void *stream) {
+    int32_t e = check_dims(d);
+    if (e != LQ_OK) return e;
+    if (state_dtype != LQ_STATE_F32 && state_dtype != LQ_STATE_BF16) return LQ_EINVAL;
+    if (d->rule != LQ_RULE_GENERAL) return LQ_EINVAL;
+    if ((e = check_ptr(S)) != LQ_OK) return e;
+    if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    if ((e = check_ptr(b)) != LQ_OK) return e;
+    lq::TokenPtrs t{q, k, v, alpha, beta, o, b};
     return hip_status(lq::launch_baseline(*d, S, state_dtype, t, (hipStream_t)stream));
 }
 

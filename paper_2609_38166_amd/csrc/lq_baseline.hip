@@ -1,6 +1,7 @@
 // Per-step baseline with a dense fp32 or bf16 state (Sec. 4.1 "Baselines"):
 //   A = D S,  u = v - A^T k,  S = A + (beta k) u^T,  o = S^T q   (Sec. 3.1)
-// (u = v for the b_t = 0 rows of the instance table, App. A)
+// (u = v for the b_t = 0 rows of the instance table, u = v - S^T b with the
+// read vector given for the general form, App. A)
 // One 256-thread workgroup per tile; 16 lanes cover one 128-entry state row
 // S^T[v][:] (8 key channels each), so both matvecs are DPP row reductions.
 // The state is read once and written once; arithmetic is fp32, a bf16 state is
@@ -44,6 +45,7 @@ struct BaseArgs {
     const float *alpha;
     const float *beta;
     float *o;
+    const float *b;   // read vectors [tiles][D] (general rule)
     int heads_v;
     int group;
 };
@@ -58,7 +60,7 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
     const size_t kvec = ((size_t)b * (a.heads_v / a.group) + hv / a.group) * D + 8 * l16;
     const size_t tvec = (size_t)tile * D;
 
-    float kx[8], qx[8], al[8], bk[8];
+    float kx[8], qx[8], al[8], bk[8], bx[8];
     const float4 *k4 = (const float4 *)(a.k + kvec);
     const float4 *q4 = (const float4 *)(a.q + kvec);
     {
@@ -77,6 +79,12 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
         const float s = a.alpha[tile];
 #pragma unroll
         for (int j = 0; j < 8; ++j) al[j] = s;
+    }
+    if (RULE == LQ_RULE_GENERAL) {
+        const float4 *b4 = (const float4 *)(a.b + tvec + 8 * l16);
+        const float4 b0 = b4[0], b1 = b4[1];
+        bx[0] = b0.x; bx[1] = b0.y; bx[2] = b0.z; bx[3] = b0.w;
+        bx[4] = b1.x; bx[5] = b1.y; bx[6] = b1.z; bx[7] = b1.w;
     }
     const float beta = a.beta[tile];
 #pragma unroll
@@ -114,11 +122,12 @@ __global__ __launch_bounds__(NT) void baseline_kernel(BaseArgs a) {
         float p = 0.0f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
+            if (RULE == LQ_RULE_GENERAL) p = fmaf(s[m][j], bx[j], p);   // S^T b (before the decay)
             s[m][j] *= al[j];                           // A = D S
-            p = fmaf(s[m][j], kx[j], p);
+            if (RULE == LQ_RULE_DELTA) p = fmaf(s[m][j], kx[j], p);     // A^T k
         }
         const float u = RULE == LQ_RULE_ADD ? a.v[tvec + vrow]
-                                            : a.v[tvec + vrow] - row16_sum(p);  // u = v - A^T k
+                                            : a.v[tvec + vrow] - row16_sum(p);  // u = v - A^T k (S^T b)
         float po = 0.0f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -157,6 +166,8 @@ template <int GATE, int BF16>
 hipError_t launch(const BaseArgs &a, int tiles, int rule, hipStream_t st) {
     if (rule == LQ_RULE_ADD)
         hipLaunchKernelGGL((baseline_kernel<GATE, BF16, LQ_RULE_ADD>), dim3(tiles), dim3(NT), 0, st, a);
+    else if (rule == LQ_RULE_GENERAL)
+        hipLaunchKernelGGL((baseline_kernel<GATE, BF16, LQ_RULE_GENERAL>), dim3(tiles), dim3(NT), 0, st, a);
     else
         hipLaunchKernelGGL((baseline_kernel<GATE, BF16, LQ_RULE_DELTA>), dim3(tiles), dim3(NT), 0, st, a);
     return hipGetLastError();
@@ -174,6 +185,7 @@ hipError_t launch_baseline(const lq_dims &d, void *S, int state_dtype, const Tok
     a.alpha = t.alpha;
     a.beta = t.beta;
     a.o = t.o;
+    a.b = t.b;
     a.heads_v = d.heads_v;
     a.group = d.heads_v / d.heads_k;
     const int tiles = d.batch * d.heads_v;

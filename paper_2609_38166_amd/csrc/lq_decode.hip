@@ -9,6 +9,9 @@
 // below -- then forms u_t = fp16(v_t - A^T k_t), the
 // output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
 // appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
+// Under the general rule (read vector b_t given, App. A) the same pass reads
+// S_{i-1}^T x, i.e. the decays Gamma_{.:i-1} without this token's, for x = b_t
+// and x = d_t . q_t (d_t the FP16 decay), and u_t = fp16(v_t - S_{i-1}^T b_t).
 //
 // Every global load of the tile is issued before the first barrier: rec_len (a
 // scalar load, which the record loads wait for), the token inputs, the
@@ -67,6 +70,7 @@ struct DecodeArgs {
     const float *alpha;
     const float *beta;
     float *o;
+    const float *b;  // read vectors [tiles][D] (general rule)
     uint64_t kv_mul; // ceil(2^32 / group), group = heads_v / heads_k
     int window;
     int n_comp;
@@ -248,13 +252,16 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     asm volatile("" : "+s"(pk), "+s"(pq), "+s"(pc), "+s"(pa), "+s"(pv), "+s"(kvm));
     using gf = const __attribute__((address_space(1))) float;
     const size_t kvec = (size_t)(((uint64_t)(uint32_t)tile * kvm) >> 32) * D;
-    float kx = 0.0f, qx = 0.0f, cs = 0.0f, vx = 0.0f;
+    const float *pb = a.b;
+    if (RULE == LQ_RULE_GENERAL) asm volatile("" : "+s"(pb));
+    float kx = 0.0f, qx = 0.0f, cs = 0.0f, vx = 0.0f, bx = 0.0f;
     if (tid < D) {
         kx = ((gf *)pk)[kvec + ch];
         qx = ((gf *)pq)[kvec + ch];
         cs = ((gf *)pc)[tvec + ch];
         if (GATE) al = ((gf *)pa)[tvec + ch];
         vx = ((gf *)pv)[tvec + ch];
+        if (RULE == LQ_RULE_GENERAL) bx = ((gf *)pb)[tvec + ch];
     }
     {
         // LDS chunk P = NT m + 64 w + L (wave w's lanes fill 1 KiB) holds chunk
@@ -289,16 +296,21 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     // a wait for one of them ahead of the code and record loads would delay
     // every load of the tile by a memory round trip.
     asm volatile("" : "+v"(kx), "+v"(qx), "+v"(cs), "+v"(al), "+v"(vx), "+v"(bt));
+    if (RULE == LQ_RULE_GENERAL) asm volatile("" : "+v"(bx));
 
     // ---- token inputs, this token's record -------------------------------------
     // carry: decay of every record newer than the current pass, channel ch
     // (the scalar gate keeps the same product in every thread below D)
     float carry = 1.0f;
     if (tid < D) {
-        s_x[0][tid] = kx;
-        s_x[1][tid] = qx;
         const uint16_t ah = f2h(al);
-        carry = h2f(ah);
+        // read vectors: k_t and q_t under the decay of this token (carry), or
+        // b_t and d_t . q_t read against S_{i-1} (carry starts at 1)
+        const bool gen = RULE == LQ_RULE_GENERAL;
+        const float xk = gen ? bx : kx, xq = gen ? h2f(ah) * qx : qx;
+        s_x[0][tid] = xk;
+        s_x[1][tid] = xq;
+        if (!gen) carry = h2f(ah);
         const size_t slot = rbase + n;
         if (GATE) a.rec_a[slot * D + ch] = ah;
         else if (tid == 0) a.rec_a[slot] = ah;
@@ -306,6 +318,8 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
         a.rec_k[slot * D + ch] = tkh;
         const float kq = wave_sum(h2f(tkh) * qx);
         if ((tid & 63) == 0) s_kq[tid >> 6] = kq;
+        kx = xk;                                             // the base vectors read these
+        qx = xq;
     }
 
     float acc_k[8], acc_q[8];
@@ -539,8 +553,9 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
             ak += s_red[w][0][idx];
             aq += s_red[w][1][idx];
         }
-        // u_t = fp16(v_t - A^T k_t); the b_t = 0 rule reads nothing (the k-side
-        // readouts above are then dead code and compiled out)
+        // u_t = fp16(v_t - A^T k_t) (general rule: v_t - S_{i-1}^T b_t); the
+        // b_t = 0 rule reads nothing (the k-side readouts above are then dead
+        // code and compiled out)
         const uint16_t uh = f2h(RULE == LQ_RULE_ADD ? vx : vx - ak);
         a.rec_u[(rbase + n) * D + ch] = uh;
         a.o[tvec + ch] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
@@ -552,6 +567,8 @@ template <int GATE, int CODE>
 hipError_t launch(const DecodeArgs &args, int rule, hipStream_t st) {
     if (rule == LQ_RULE_ADD)
         hipLaunchKernelGGL((decode_kernel<GATE, CODE, LQ_RULE_ADD>), dim3(args.tiles), dim3(NT), 0, st, args);
+    else if (rule == LQ_RULE_GENERAL)
+        hipLaunchKernelGGL((decode_kernel<GATE, CODE, LQ_RULE_GENERAL>), dim3(args.tiles), dim3(NT), 0, st, args);
     else
         hipLaunchKernelGGL((decode_kernel<GATE, CODE, LQ_RULE_DELTA>), dim3(args.tiles), dim3(NT), 0, st, args);
     return hipGetLastError();
@@ -577,6 +594,7 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
     a.alpha = t.alpha;
     a.beta = t.beta;
     a.o = t.o;
+    a.b = t.b;
     const uint64_t group = (uint64_t)(d.heads_v / d.heads_k);
     a.kv_mul = ((1ull << 32) + group - 1) / group;
     a.window = d.window;

@@ -28,6 +28,7 @@ struct TokenPtrs {
     const float *alpha;
     const float *beta;
     float *o;
+    const float *b;     // read vectors [tiles][d_k] (general rule only, else null)
 };
 
 hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &t, hipStream_t st);

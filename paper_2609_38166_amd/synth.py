@@ -50,7 +50,7 @@ class Workload:
     prefill: int = 512        # tokens of the unquantized prefill that builds the initial state
     power_iters: int = 4
     smooth: int = 1           # residual smoothing on (1) or c = 1 (0)
-    rule: int = 0             # read vector of the recurrence: delta rule (0) or b_t = 0 (1)
+    rule: int = 0             # read vector: delta rule (0), b_t = 0 (1), given with the token (2)
     outliers: str = "all"     # "all": every tile; "frac": 5 % of tiles; "none"
     outlier_factor: float = 20.0
     seed: int = 20260000

@@ -28,21 +28,19 @@ def rwkv7_raw(rng: np.random.Generator, tiles: int, T: int, dk: int, dv: int) ->
     """Per-token RWKV7 inputs, [tiles][T][...] float32: decay w = exp(-e^-0.5
     sigmoid(z)) in (0.545, 1) per key channel, in-context rate a = sigmoid(z),
     removal key kappa, key k and receptance r unit-norm Gaussian, value v
-    ~ N(0, I)."""
-    def unit(shape):
-        x = rng.standard_normal(shape)
-        return (x / np.linalg.norm(x, axis=-1, keepdims=True)).astype(np.float32)
-
-    def sig(x):
-        return 1.0 / (1.0 + np.exp(-x))
-
+    ~ N(0, I).  One draw of 5 x d_k + d_v normals per token."""
+    z = rng.standard_normal((tiles, T, 5 * dk + dv), dtype=np.float32)
+    zk = z[..., :5 * dk].reshape(tiles, T, 5, dk)
+    one = np.float32(1.0)
+    sig = one / (one + np.exp(-zk[:, :, :2]))
+    unit = zk[:, :, 2:] / np.sqrt(np.einsum("tsjd,tsjd->tsj", zk[:, :, 2:], zk[:, :, 2:]))[..., None]
     return {
-        "w": np.exp(-np.exp(-0.5) * sig(rng.standard_normal((tiles, T, dk)))).astype(np.float32),
-        "a": sig(rng.standard_normal((tiles, T, dk))).astype(np.float32),
-        "kappa": unit((tiles, T, dk)),
-        "k": unit((tiles, T, dk)),
-        "r": unit((tiles, T, dk)),
-        "v": rng.standard_normal((tiles, T, dv)).astype(np.float32),
+        "w": np.exp(np.float32(-np.exp(-0.5)) * sig[:, :, 0]),
+        "a": np.ascontiguousarray(sig[:, :, 1]),
+        "kappa": np.ascontiguousarray(unit[:, :, 0]),
+        "k": np.ascontiguousarray(unit[:, :, 1]),
+        "r": np.ascontiguousarray(unit[:, :, 2]),
+        "v": np.ascontiguousarray(z[..., 5 * dk:]),
     }
 
 

@@ -95,6 +95,35 @@ def test_validation_rejects_bad_arguments_before_launch():
     assert _call_decode(d0, st0, toks) == B.LQ_EUNSUPPORTED   # dims checked first
 
 
+def test_general_rule_entry_points_validate_rule_and_read_vectors():
+    """The general rule has entry points of its own: the plain steps reject it,
+    the general steps require it and a valid read-vector pointer."""
+    good = 0x10000
+    st = B.lq_state(*([good] * 10))
+    toks = [good] * 6
+    L = B.lib()
+    dg = B.make_dims(2, 4, heads_k=2, rule=B.LQ_RULE_GENERAL)
+    dd = B.make_dims(2, 4, heads_k=2, rule=B.LQ_RULE_DELTA)
+    assert _call_decode(dg, st, toks) == B.LQ_EINVAL
+    assert L.leapquant_baseline_step(C.byref(dg), good, B.LQ_STATE_F32, *toks, None) == B.LQ_EINVAL
+
+    def dec(d, b):
+        q, k, v, a, be, o = toks
+        return L.leapquant_decode_step_general(C.byref(d), C.byref(st), q, k, b, v, a, be, o, None)
+
+    def base(d, b, dtype=B.LQ_STATE_F32):
+        q, k, v, a, be, o = toks
+        return L.leapquant_baseline_step_general(C.byref(d), good, dtype, q, k, b, v, a, be, o, None)
+
+    for fn in (dec, base):
+        assert fn(dd, good) == B.LQ_EINVAL                          # rule is not GENERAL
+        assert fn(B.make_dims(2, 4, heads_k=2, rule=B.LQ_RULE_ADD), good) == B.LQ_EINVAL
+        assert fn(dg, None) == B.LQ_EINVAL                          # read vectors missing
+        assert fn(dg, good + 8) == B.LQ_EALIGN
+        assert fn(B.make_dims(2, 4, heads_k=2, rule=3), good) == B.LQ_EINVAL
+    assert base(dg, good, dtype=5) == B.LQ_EINVAL
+
+
 def test_strerror_covers_every_status():
     for s in (B.LQ_OK, B.LQ_EINVAL, B.LQ_EALIGN, B.LQ_EUNSUPPORTED, B.LQ_EHIP, B.LQ_EDEVICE):
         assert B.strerror(s) and B.strerror(s) != "unknown status"

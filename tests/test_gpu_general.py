@@ -1,0 +1,222 @@
+"""GPU parity of the general read-vector rule (App. A) against the CPU oracle.
+
+RWKV7 runs as two sub-steps per token (erase with b = a . kappa, then a pure
+write; per-channel gate), and the scalar gate is driven with read vectors drawn
+independently of the keys, over a window longer than one pass of the decode's
+record loop.  Calls go through leapquant_decode_step_general and
+leapquant_baseline_step_general; the bars are those of the delta-rule tests
+(window-synchronised protocol, gpu_harness.window_protocol).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_38166_amd import binding as B
+from paper_2609_38166_amd import synth
+from tests import gpu_harness as H
+from tests import instances
+
+pytestmark = pytest.mark.gpu
+
+GEN = synth.WORKLOADS["kda_kimi"].with_(rule=O.RULE_GENERAL)
+CASES = {
+    # RWKV7 sub-steps, W counts sub-steps; windows end between the two halves of a token
+    "rwkv7_w16_r4": GEN.with_(name="rwkv7_w16_r4", batch=2, heads_v=4, heads_k=4, steps=80, window=16,
+                              n_comp=4),
+    "rwkv7_w64_e4m3": GEN.with_(name="rwkv7_w64_e4m3", batch=2, heads_v=4, heads_k=4, steps=128,
+                                window=64, n_comp=8, code=synth.CODE_E4M3),
+    "rwkv7_w21_int4": GEN.with_(name="rwkv7_w21_int4", batch=2, heads_v=4, heads_k=4, steps=84,
+                                window=21, n_comp=8, code=synth.CODE_INT4),
+    # scalar gate, arbitrary read vectors, 100 records per window (two record passes)
+    "general_gdn_w100": GEN.with_(name="general_gdn_w100", batch=2, heads_v=4, heads_k=4, steps=200,
+                                  window=100, n_comp=8, gate=synth.GATE_SCALAR),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _tile_substeps(wl, T, rng):
+    """One tile's sub-step stream [1][T][...] with read vectors."""
+    if wl.gate == synth.GATE_DIAG:
+        return instances.rwkv7_substeps(instances.rwkv7_raw(rng, 1, T // 2, wl.dk, wl.dv))
+    q = rng.standard_normal((1, T, wl.dk))
+    k = rng.standard_normal((1, T, wl.dk))
+    b = rng.standard_normal((1, T, wl.dk))
+    unit = lambda x: (x / np.linalg.norm(x, axis=-1, keepdims=True)).astype(np.float32)
+    return {"q": unit(q), "k": unit(k), "v": rng.standard_normal((1, T, wl.dv)).astype(np.float32),
+            "b": (unit(b) * rng.uniform(0.3, 1.0, (1, T, 1))).astype(np.float32),
+            "alpha": np.exp(-0.1 * np.logaddexp(0, rng.standard_normal((1, T, 1)))).astype(np.float32),
+            "beta": (1 / (1 + np.exp(-rng.standard_normal((1, T))))).astype(np.float32)}
+
+
+def _substeps(wl, T, seed, tiles=None):
+    """Oracle-layout sub-step streams [tiles][T][...] with read vectors; every
+    tile draws from its own generator, so a sample of tiles gets the same
+    values as the full batch."""
+    tiles = range(wl.tiles) if tiles is None else tiles
+    parts = [_tile_substeps(wl, T, np.random.default_rng([wl.seed, seed, int(t)])) for t in tiles]
+    return {n: np.concatenate([p[n] for p in parts]) for n in parts[0]}
+
+
+class _Dev:
+    """Step-major device copies of an oracle-layout sub-step stream."""
+
+    def __init__(self, wl, tok):
+        sm = lambda n: H.dev(instances.step_major(tok[n], wl.batch, wl.heads_v))
+        self.q, self.k, self.b, self.v, self.beta = (sm(n) for n in ("q", "k", "b", "v", "beta"))
+        a = instances.step_major(tok["alpha"], wl.batch, wl.heads_v)
+        self.alpha = H.dev(a if wl.gate == synth.GATE_DIAG else a[..., 0])
+
+    def step(self, t):
+        return self.q[t], self.k[t], self.b[t], self.v[t], self.alpha[t], self.beta[t]
+
+
+class _DevSampled(_Dev):
+    """Full-batch RWKV7 sub-step inputs for launches over every tile: drawn on
+    the device for the tiles no oracle looks at (same recipe, torch's
+    generator), with the sampled tiles' host streams written over their rows."""
+
+    def __init__(self, wl, tok_sample, sample, T, seed):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        n, shp = T // 2, (T // 2, wl.batch, wl.heads_v, wl.dk)
+        rnd = lambda shape=shp: torch.randn(shape, generator=g, device="cuda")
+
+        def unit():
+            x = rnd()
+            return x / x.norm(dim=-1, keepdim=True)
+
+        def inter(x0, x1):
+            out = torch.empty((2 * n,) + tuple(x0.shape[1:]), device="cuda")
+            out[0::2], out[1::2] = x0, x1
+            return out.contiguous()
+
+        w = torch.exp(-np.exp(-0.5) * torch.sigmoid(rnd()))
+        a = torch.sigmoid(rnd())
+        kap, k, r = unit(), unit(), unit()
+        v = rnd((n, wl.batch, wl.heads_v, wl.dv))
+        zero = torch.zeros(shp, device="cuda")
+        self.q, self.k, self.b = inter(r, r), inter(kap, k), inter(a * kap, zero)
+        self.v, self.alpha = inter(torch.zeros_like(v), v), inter(w, torch.ones(shp, device="cuda"))
+        self.beta = torch.ones((2 * n, wl.batch, wl.heads_v), device="cuda")
+        idx = torch.as_tensor(np.asarray(sample, np.int64), device="cuda")
+        for name in ("q", "k", "b", "v", "alpha", "beta"):
+            dst = getattr(self, name)
+            flat = dst.view((T, wl.tiles) + tuple(dst.shape[3:]))
+            flat[:, idx] = H.dev(np.moveaxis(tok_sample[name], 1, 0))
+
+
+def _initial_state(wl, seed, tiles=None):
+    """fp32 recurrence over a 256-step prefill of the same kind of stream from
+    zero, then the workload's outlier lines (oracle layout)."""
+    pre = _substeps(wl, 256, seed + 1000, tiles)
+    n = len(pre["q"])
+    _, Sp = O.run_baseline(H.ocfg(wl), np.zeros((n, wl.dk, wl.dv)), pre, mode=O.STATE_F32, want_o=False)
+    F = synth.outlier_factor(synth.outliers(wl, tiles))
+    return (Sp.astype(np.float32) * F).astype(np.float64)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_general_rule_window_parity(name):
+    wl = CASES[name]
+    H.log(f"general rule, {name}")
+    cfg, dims = H.ocfg(wl), H.gdims(wl)
+    S0 = _initial_state(wl, 1)
+    tok = _substeps(wl, wl.steps, 2)
+    ref = O.run_dense(cfg, S0, tok, snapshots=True, history=True)
+    dt = _Dev(wl, tok)
+
+    def decode(st, t, o):
+        B.leapquant_decode_step_general(dims, st, *dt.step(t), o)
+
+    H.window_protocol(name, cfg, dims, ref, wl.steps, decode)
+
+
+def test_general_rule_full_size_sampled():
+    """RWKV7 sub-steps at the KDA layer's full size (256 requests x 32 heads,
+    W = 64 sub-steps, r = 8, int8): every launch covers all 8192 tiles, a seeded
+    sample of 32 tiles is compared with the oracle."""
+    wl = GEN.with_(name="rwkv7_full", steps=64)
+    vt = H.sample_tiles(wl, 32)
+    cfg, dims = H.ocfg(wl), H.gdims(wl)
+    S0 = _initial_state(wl, 1, vt)
+    tok = _substeps(wl, wl.steps, 2, vt)
+    ref = O.run_dense(cfg, S0, tok, snapshots=True, history=True)
+    H.log(f"[{wl.name}] oracle done on {len(vt)} of {wl.tiles} tiles")
+    dt = _DevSampled(wl, tok, vt, wl.steps, wl.seed)
+
+    def decode(st, t, o):
+        B.leapquant_decode_step_general(dims, st, *dt.step(t), o)
+
+    H.window_protocol(wl.name, cfg, dims, ref, wl.steps, decode, sample=vt,
+                      fill=lambda st: H.filler_state(st, wl))
+
+
+def test_rwkv7_write_substep_through_the_additive_call():
+    """The write half of an RWKV7 token may go through leapquant_decode_step on
+    the same state with the additive rule instead of the general call with
+    b = 0, alpha = 1: identical records and outputs, bit for bit."""
+    wl = CASES["rwkv7_w16_r4"]
+    dims_g = H.gdims(wl)
+    dims_a = H.gdims(wl, rule=B.LQ_RULE_ADD)
+    tok = _substeps(wl, 32, 3)
+    dt = _Dev(wl, tok)
+    S0 = H.dev(np.ascontiguousarray(_initial_state(wl, 3).transpose(0, 2, 1)).astype(np.float32))
+    outs = {}
+    for mode in ("general", "mixed"):
+        st = B.State.empty(dims_g)
+        B.leapquant_quantize_state(dims_g, S0, st)
+        o = torch.empty((wl.batch, wl.heads_v, wl.dv), device="cuda")
+        got = []
+        for t in range(32):
+            q, k, b, v, a, be = dt.step(t)
+            if mode == "mixed" and t % 2 == 1:
+                B.leapquant_decode_step(dims_a, st, q, k, v, a, be, o)
+            else:
+                B.leapquant_decode_step_general(dims_g, st, q, k, b, v, a, be, o)
+            got.append(o.clone())
+            if (t + 1) % wl.window == 0:
+                B.leapquant_window_commit(dims_g, st)
+        torch.cuda.synchronize()
+        outs[mode] = (torch.stack(got), {f: getattr(st, f).clone() for f in B.FIELDS})
+        assert B.leapquant_check_error(st) == 0
+    assert torch.equal(outs["general"][0], outs["mixed"][0])
+    for f in B.FIELDS:
+        assert torch.equal(outs["general"][1][f], outs["mixed"][1][f]), f
+
+
+@pytest.mark.parametrize("gate", [synth.GATE_SCALAR, synth.GATE_DIAG])
+@pytest.mark.parametrize("dtype", [B.LQ_STATE_F32, B.LQ_STATE_BF16])
+def test_baseline_step_general_parity(gate, dtype):
+    wl = CASES["rwkv7_w16_r4" if gate == synth.GATE_DIAG else "general_gdn_w100"]
+    H.log(f"baseline general gate={gate} dtype={dtype}")
+    rng = np.random.default_rng(9)
+    S0 = rng.standard_normal((wl.tiles, wl.dk, wl.dv)).astype(np.float32).astype(np.float64)
+    if dtype == B.LQ_STATE_BF16:
+        S0 = (O.f32_to_bf16_bits(S0.astype(np.float32)).astype(np.uint32) << 16).view(np.float32)
+        S0 = S0.astype(np.float64)
+    tok = _substeps(wl, 24, 4)
+    o_ref, S_ref = O.run_baseline(H.ocfg(wl), S0, tok,
+                                  mode=O.STATE_F32 if dtype == B.LQ_STATE_F32 else O.STATE_BF16)
+    dims = H.gdims(wl)
+    S_t = np.ascontiguousarray(S0.transpose(0, 2, 1)).astype(np.float32)
+    S_g = H.dev(S_t).to(torch.bfloat16) if dtype == B.LQ_STATE_BF16 else H.dev(S_t)
+    dt = _Dev(wl, tok)
+    o = torch.empty((wl.tiles, wl.dv), dtype=torch.float32, device="cuda")
+    outs = []
+    for t in range(24):
+        B.leapquant_baseline_step_general(dims, S_g, dtype, *dt.step(t), o)
+        outs.append(o.cpu().numpy())
+    og = np.stack(outs, axis=1)
+    Sg = S_g.float().cpu().numpy().transpose(0, 2, 1)
+    tol = 1e-5 if dtype == B.LQ_STATE_F32 else 2e-3
+    assert H.rel_rows(og, o_ref) < tol
+    assert H.rel_rows(Sg.reshape(wl.tiles, -1), S_ref.reshape(wl.tiles, -1)) < tol
