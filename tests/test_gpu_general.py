@@ -1,10 +1,13 @@
-"""GPU parity of the general read-vector rule (App. A) against the CPU oracle.
+"""GPU parity of the instances that split a token into sub-steps, and of the
+general read-vector rule (App. A), against the CPU oracle.
 
 RWKV7 runs as two sub-steps per token (erase with b = a . kappa, then a pure
 write; per-channel gate), and the scalar gate is driven with read vectors drawn
 independently of the keys, over a window longer than one pass of the decode's
-record loop.  Calls go through leapquant_decode_step_general and
-leapquant_baseline_step_general; the bars are those of the delta-rule tests
+record loop; these calls go through leapquant_decode_step_general and
+leapquant_baseline_step_general.  DeltaProduct (n delta-rule sub-steps per
+token, the token's gate on the first) and DeltaNet (alpha = 1) go through the
+plain delta-rule call.  The bars are those of the delta-rule tests
 (window-synchronised protocol, gpu_harness.window_protocol).
 """
 import numpy as np
@@ -220,3 +223,56 @@ def test_baseline_step_general_parity(gate, dtype):
     tol = 1e-5 if dtype == B.LQ_STATE_F32 else 2e-3
     assert H.rel_rows(og, o_ref) < tol
     assert H.rel_rows(Sg.reshape(wl.tiles, -1), S_ref.reshape(wl.tiles, -1)) < tol
+
+
+DP = synth.WORKLOADS["gdn_tiny"]
+DP_CASES = {
+    # DeltaProduct, n = 3 sub-steps per token, W = 48 sub-steps (16 tokens), beta in [0, 2]
+    "deltaproduct_n3_w48": (DP.with_(name="deltaproduct_n3_w48", steps=96, window=48, n_comp=4), 3),
+    # DeltaNet: D = I (alpha = 1 on every step)
+    "deltanet_w16": (DP.with_(name="deltanet_w16", steps=64, window=16, n_comp=4), 1),
+}
+
+
+def _dp_substeps(wl, n, seed, tiles):
+    """DeltaProduct sub-steps per tile: unit q, k, v ~ N(0, I), beta ~ U[0, 2],
+    the token's scalar gate exp(-0.1 softplus(z)) on its first sub-step (n = 1:
+    DeltaNet, alpha = 1 throughout)."""
+    parts = []
+    for t in tiles:
+        rng = np.random.default_rng([wl.seed, seed, int(t)])
+        T = wl.steps
+        q = rng.standard_normal((1, T, wl.dk))
+        k = rng.standard_normal((1, T, wl.dk))
+        sub = {"q": (q / np.linalg.norm(q, axis=-1, keepdims=True)).astype(np.float32),
+               "k": (k / np.linalg.norm(k, axis=-1, keepdims=True)).astype(np.float32),
+               "v": rng.standard_normal((1, T, wl.dv)).astype(np.float32),
+               "beta": rng.uniform(0.0, 2.0, (1, T)).astype(np.float32)}
+        if n == 1:
+            sub["alpha"] = np.ones((1, T, 1), np.float32)
+            parts.append(sub)
+        else:
+            sub["alpha"] = np.exp(-0.1 * np.logaddexp(0, rng.standard_normal((1, T // n, 1)))).astype(np.float32)
+            parts.append(instances.deltaproduct_substeps(sub, n))
+    return {k_: np.concatenate([p_[k_] for p_ in parts]) for k_ in parts[0]}
+
+
+@pytest.mark.parametrize("name", list(DP_CASES))
+def test_deltaproduct_and_deltanet_window_parity(name):
+    wl, n = DP_CASES[name]
+    H.log(f"sub-step instance {name}")
+    cfg, dims = H.ocfg(wl), H.gdims(wl)
+    rng = np.random.default_rng([wl.seed, 5])
+    S0 = np.stack([np.outer(rng.standard_normal(wl.dk), rng.standard_normal(wl.dv)) * 0.5
+                   + 0.1 * rng.standard_normal((wl.dk, wl.dv)) for _ in range(wl.tiles)])
+    S0 = (S0.astype(np.float32) * synth.outlier_factor(synth.outliers(wl))).astype(np.float64)
+    tok = _dp_substeps(wl, n, 6, range(wl.tiles))
+    ref = O.run_dense(cfg, S0, tok, snapshots=True, history=True)
+    sm = {k_: H.dev(instances.step_major(v_, wl.batch, wl.heads_v)) for k_, v_ in tok.items()}
+    sm["alpha"] = sm["alpha"][..., 0].contiguous()
+
+    def decode(st, t, o):
+        B.leapquant_decode_step(dims, st, sm["q"][t], sm["k"][t], sm["v"][t], sm["alpha"][t],
+                                sm["beta"][t], o)
+
+    H.window_protocol(name, cfg, dims, ref, wl.steps, decode)
