@@ -139,6 +139,8 @@ int32_t leapquant_state_bytes(const lq_dims *dims, size_t bytes_out[10]);
  * delta_v = max_k |R^C_kv| / 127, code = clamp(rint(R^C * 127/max), +-127).
  * The 6- and 4-bit variants (the paper's lower-bit LeapQuant, Sec. 4.1-4.2)
  * use the same rule with qmax = 31 and 7 (2^(b-1) - 1) and packed storage.
+ * The fit, the deflation and the smoothing statistic are carried in fp64;
+ * the FP16 rounding of the tokens and the codes are decided in fp32.
  */
 int32_t leapquant_quantize_state(const lq_dims *dims, const float *S, lq_state *st, void *stream);
 
@@ -194,7 +196,7 @@ int32_t leapquant_decode_step_general(const lq_dims *dims, lq_state *st, const f
  *         NULL = commit all requests.
  * For a selected tile with p = rec_len > 0 records, reconstruct
  *   S_p = Gamma_{1:p} [C dequant(Z) + K~ U~^T] + sum_j Gamma_{j+1:p} k~_j u_j^T
- * in fp32, discard the old tokens, re-quantize S_p exactly as
+ * in fp64, discard the old tokens, re-quantize S_p exactly as
  * leapquant_quantize_state does and set rec_len = 0.  A partial window
  * (p < W) is legal; tiles with rec_len == 0 or an unselected request are left
  * untouched.
