@@ -34,6 +34,9 @@ CASES = {
     # scalar gate, arbitrary read vectors, 100 records per window (two record passes)
     "general_gdn_w100": GEN.with_(name="general_gdn_w100", batch=2, heads_v=4, heads_k=4, steps=200,
                                   window=100, n_comp=8, gate=synth.GATE_SCALAR),
+    # grouped keys: two value heads per key head, read vectors per value head
+    "general_gqa_w32": GEN.with_(name="general_gqa_w32", batch=2, heads_v=4, heads_k=2, steps=64,
+                                 window=32, n_comp=4, gate=synth.GATE_SCALAR),
 }
 
 
@@ -63,9 +66,17 @@ def _tile_substeps(wl, T, rng):
 def _substeps(wl, T, seed, tiles=None):
     """Oracle-layout sub-step streams [tiles][T][...] with read vectors; every
     tile draws from its own generator, so a sample of tiles gets the same
-    values as the full batch."""
+    values as the full batch.  With grouped keys, the value heads of a group
+    take q and k from the group's first value head."""
     tiles = range(wl.tiles) if tiles is None else tiles
-    parts = [_tile_substeps(wl, T, np.random.default_rng([wl.seed, seed, int(t)])) for t in tiles]
+    group = wl.heads_v // wl.heads_k
+    parts = []
+    for t in tiles:
+        p = _tile_substeps(wl, T, np.random.default_rng([wl.seed, seed, int(t)]))
+        if group > 1 and t % group:
+            lead = _tile_substeps(wl, T, np.random.default_rng([wl.seed, seed, int(t) - int(t) % group]))
+            p["q"], p["k"] = lead["q"], lead["k"]
+        parts.append(p)
     return {n: np.concatenate([p[n] for p in parts]) for n in parts[0]}
 
 
@@ -74,7 +85,10 @@ class _Dev:
 
     def __init__(self, wl, tok):
         sm = lambda n: H.dev(instances.step_major(tok[n], wl.batch, wl.heads_v))
-        self.q, self.k, self.b, self.v, self.beta = (sm(n) for n in ("q", "k", "b", "v", "beta"))
+        self.b, self.v, self.beta = (sm(n) for n in ("b", "v", "beta"))
+        group = wl.heads_v // wl.heads_k             # one q, k row per key head
+        self.q, self.k = (H.dev(instances.step_major(tok[n], wl.batch, wl.heads_v)[:, :, ::group])
+                          for n in ("q", "k"))
         a = instances.step_major(tok["alpha"], wl.batch, wl.heads_v)
         self.alpha = H.dev(a if wl.gate == synth.GATE_DIAG else a[..., 0])
 
