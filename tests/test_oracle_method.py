@@ -444,15 +444,18 @@ def _tokens(rng, tiles, T, dk, dv, gate):
 
 @pytest.mark.parametrize("gate", [0, 1])
 @pytest.mark.parametrize("W", [1, 3, 16])
-@pytest.mark.parametrize("rule", [0, 1])
+@pytest.mark.parametrize("rule", [0, 1, 2])
 def test_window_unrolling_equals_recurrence(O, gate, W, rule):
     """Quantization off and exact records: the per-window method (both forms) is
     the recurrence itself (Eq. (window) follows from Eq. (record) by induction),
-    for the delta rule and for the b_t = 0 rows of the instance table."""
+    for the delta rule, the b_t = 0 rows of the instance table and the general
+    read vector."""
     rng = np.random.default_rng(50 + W + gate + 7 * rule)
     dk = dv = 32
     S0 = rng.standard_normal((3, dk, dv))
     tok = _tokens(rng, 3, 37, dk, dv, gate)
+    if rule == 2:
+        tok["b"] = f32(0.7 * rng.standard_normal((3, 37, dk)) / np.sqrt(dk))
     cfg = O.make_cfg(dk=dk, dv=dv, window=W, n_comp=2, gate=gate, quantize=0, round_records=0,
                      rule=rule)
     o_ref, S_ref = O.run_baseline(cfg, S0, tok, mode=O.STATE_EXACT)
