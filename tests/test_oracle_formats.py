@@ -2,7 +2,6 @@
 format definitions (binary16 via numpy, bfloat16 and E4M3FN via torch, E4M3FN
 decode values from the OCP 8-bit floating point specification)."""
 import numpy as np
-import pytest
 import torch
 
 
