@@ -34,6 +34,9 @@ CASES = {
     # scalar gate, arbitrary read vectors, 100 records per window (two record passes)
     "general_gdn_w100": GEN.with_(name="general_gdn_w100", batch=2, heads_v=4, heads_k=4, steps=200,
                                   window=100, n_comp=8, gate=synth.GATE_SCALAR),
+    # per-step requantization without tokens or smoothing (W = 1, r = 0): every sub-step commits
+    "rwkv7_w1_r0": GEN.with_(name="rwkv7_w1_r0", batch=2, heads_v=4, heads_k=4, steps=12, window=1,
+                             n_comp=0, smooth=0),
     # grouped keys: two value heads per key head, read vectors per value head
     "general_gqa_w32": GEN.with_(name="general_gqa_w32", batch=2, heads_v=4, heads_k=2, steps=64,
                                  window=32, n_comp=4, gate=synth.GATE_SCALAR),
