@@ -361,6 +361,76 @@ def decode_two_batches(wl, dims, S0, toks, reps=3):
     return float(np.mean(ts))
 
 
+def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3):
+    """Average time per decode step over one window cycle (W steps, one commit
+    per request) when the requests are split into G groups whose windows are
+    offset by W/G steps, each group on its own stream (its commit follows its
+    own decode; the other groups' decodes can run beside it), replayed as one
+    graph.  G = 1 is the aligned schedule of the headline step."""
+    import torch
+    from paper_2609_38166_amd import binding as B_
+    W, Bt = wl.window, wl.batch
+    q, k, v, a, b = toks
+    st = B_.State.empty(dims)
+    o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+
+    def sub(b0, b1):
+        d = B_.make_dims(b1 - b0, wl.heads_v, wl.heads_k, window=W, n_comp=wl.n_comp,
+                         power_iters=wl.power_iters, gate=wl.gate, code=wl.code)
+        return d, B_.State(d, *[getattr(st, f)[b0:b1] if f != "err" else st.err for f in B_.FIELDS])
+
+    res = {}
+    for G in groups:
+        R = Bt // G
+        parts = [(gi * R, (gi + 1) * R, (gi * W // G) % W) + sub(gi * R, (gi + 1) * R) for gi in range(G)]
+        streams = [torch.cuda.Stream() for _ in range(G)]
+
+        def cycle():
+            main = torch.cuda.current_stream()
+            for s_ in streams:
+                s_.wait_stream(main)
+            for t in range(W):
+                for (b0, b1, off, d, sv), s_ in zip(parts, streams):
+                    with torch.cuda.stream(s_):
+                        B_.leapquant_decode_step(d, sv, q[t][b0:b1], k[t][b0:b1], v[t][b0:b1], a[t][b0:b1],
+                                                 b[t][b0:b1], o[b0:b1])
+                        if (t + 1 + off) % W == 0:
+                            B_.leapquant_window_commit(d, sv)
+            for s_ in streams:
+                main.wait_stream(s_)
+
+        def reset():
+            B_.leapquant_quantize_state(dims, S0, st)
+            for b0, b1, off, _, _ in parts:
+                st.rec_len[b0:b1] = off
+
+        reset()
+        cycle()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        reset()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            cycle()
+        ts = []
+        for rep in range(reps + 1):
+            reset()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                ts.append(e0.elapsed_time(e1) / W)
+        if B_.leapquant_check_error(st):
+            raise RuntimeError("device error during the staggered-window timing")
+        res[f"G{G}_us_per_step"] = round(float(np.mean(ts)) * 1e3, 2)
+        del g
+    del st
+    return res
+
+
 def copy_calibration(nbytes=1 << 30):
     """One plain device-to-device copy of known size, for scaling the HBM byte
     counters of a profiler run (FETCH_SIZE / WRITE_SIZE of this dispatch are
@@ -591,6 +661,11 @@ def main():
         "avg_launch_us": round(two * 1e3, 2), "achieved": round(dec_avg_bytes / (two * 1e-3) / 1e9, 1),
         "note": "two batches alternate, so no batch's codes stay in the Infinity Cache between its steps"}
     log(f"[bench] decode with two alternating batches {two * 1e3:.1f} us/launch")
+    if not args.no_variants:
+        out["staggered_windows"] = staggered_windows(wl, dims, S0, toks)
+        out["staggered_windows"]["note"] = ("requests in G groups whose windows are offset by W/G, one stream "
+                                            "per group; per decode step over one window cycle incl. commits")
+        log(f"[bench] staggered windows {out['staggered_windows']}")
     ceil = stream_read_ceiling()
     out["stream_read_ceiling"] = ceil
     out["roofline"]["frac_of_stream_ceiling"] = round(achieved / ceil["gbps"], 4)
