@@ -16,7 +16,9 @@
  *  - One tile = one (request b, value head h) pair; tiles are numbered
  *    b * heads_v + h.  d_k = d_v = 128 in this version.
  *  - Every array argument is a caller-owned DEVICE pointer, dense, row-major,
- *    16-byte aligned.  The library allocates no memory, keeps no global state
+ *    16-byte aligned, except the per-tile scalars beta and (scalar gate) alpha,
+ *    which need 4-byte alignment only (so one step of a step-major buffer can
+ *    be passed for any tile count).  The library allocates no memory, keeps no global state
  *    and never synchronises (except leapquant_check_error).  Work is enqueued on
  *    `stream` (a hipStream_t; NULL = the default stream) and returns at once.
  *    Calls on different streams with disjoint buffers may run concurrently.
@@ -44,7 +46,7 @@ extern "C" {
 /* ---- status codes ---- */
 #define LQ_OK            0
 #define LQ_EINVAL       -1   /* NULL pointer, non-positive size, inconsistent heads   */
-#define LQ_EALIGN       -2   /* a pointer is not 16-byte aligned                      */
+#define LQ_EALIGN       -2   /* a pointer is not aligned (16 bytes; 4 for beta / alpha) */
 #define LQ_EUNSUPPORTED -3   /* d_k/d_v != 128, r > 16, W out of range, ...           */
 #define LQ_EHIP         -4   /* a HIP call failed (kernel launch, synchronisation)    */
 #define LQ_EDEVICE      -5   /* a sticky device error was found by check_error        */

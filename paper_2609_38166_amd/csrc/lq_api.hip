@@ -70,10 +70,22 @@ int32_t check_state(const lq_dims *d, const lq_state *st) {
     return LQ_OK;
 }
 
-int32_t check_tokens(const float *q, const float *k, const float *v, const float *alpha,
-                     const float *beta, const float *o) {
+// Per-tile scalar arrays (beta, and alpha under the scalar gate) are read one
+// word at a time and need only 4-byte alignment, so that step-major buffers of
+// any tile count can be passed one step at a time; every other array is read
+// in 16-byte vectors by some kernel.
+int32_t check_ptr4(const void *p) {
+    if (!p) return LQ_EINVAL;
+    if ((uintptr_t)p & 3u) return LQ_EALIGN;
+    return LQ_OK;
+}
+
+int32_t check_tokens(const lq_dims *d, const float *q, const float *k, const float *v,
+                     const float *alpha, const float *beta, const float *o) {
     int32_t e;
-    const void *ptrs[] = {q, k, v, alpha, beta, o};
+    if ((e = d->gate == LQ_GATE_DIAG ? check_ptr(alpha) : check_ptr4(alpha)) != LQ_OK) return e;
+    if ((e = check_ptr4(beta)) != LQ_OK) return e;
+    const void *ptrs[] = {q, k, v, o};
     for (const void *p : ptrs)
         if ((e = check_ptr(p)) != LQ_OK) return e;
     return LQ_OK;
@@ -134,7 +146,7 @@ int32_t leapquant_decode_step(const lq_dims *d, lq_state *st, const float *q, co
     if (e != LQ_OK) return e;
     if ((e = check_state(d, st)) != LQ_OK) return e;
     if (d->rule == LQ_RULE_GENERAL) return LQ_EINVAL;   // needs the read vectors
-    if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    if ((e = check_tokens(d, q, k, v, alpha, beta, o)) != LQ_OK) return e;
     lq::TokenPtrs t{q, k, v, alpha, beta, o, nullptr};
     return hip_status(lq::launch_decode(*d, state_ptrs(st), t, (hipStream_t)stream));
 }
@@ -147,7 +159,7 @@ int32_t leapquant_decode_step_general(const lq_dims *d, lq_state *st, const floa
     if (e != LQ_OK) return e;
     if ((e = check_state(d, st)) != LQ_OK) return e;
     if (d->rule != LQ_RULE_GENERAL) return LQ_EINVAL;
-    if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    if ((e = check_tokens(d, q, k, v, alpha, beta, o)) != LQ_OK) return e;
     if ((e = check_ptr(b)) != LQ_OK) return e;
     lq::TokenPtrs t{q, k, v, alpha, beta, o, b};
     return hip_status(lq::launch_decode(*d, state_ptrs(st), t, (hipStream_t)stream));
@@ -170,7 +182,7 @@ int32_t leapquant_baseline_step(const lq_dims *d, void *S, int32_t state_dtype, 
     if (state_dtype != LQ_STATE_F32 && state_dtype != LQ_STATE_BF16) return LQ_EINVAL;
     if ((e = check_ptr(S)) != LQ_OK) return e;
     if (d->rule == LQ_RULE_GENERAL) return LQ_EINVAL;   // needs the read vectors
-    if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    if ((e = check_tokens(d, q, k, v, alpha, beta, o)) != LQ_OK) return e;
     lq::TokenPtrs t{q, k, v, alpha, beta, o, nullptr};
     return hip_status(lq::launch_baseline(*d, S, state_dtype, t, (hipStream_t)stream));
 }
@@ -184,7 +196,7 @@ int32_t leapquant_baseline_step_general(const lq_dims *d, void *S, int32_t state
     if (state_dtype != LQ_STATE_F32 && state_dtype != LQ_STATE_BF16) return LQ_EINVAL;
     if (d->rule != LQ_RULE_GENERAL) return LQ_EINVAL;
     if ((e = check_ptr(S)) != LQ_OK) return e;
-    if ((e = check_tokens(q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    if ((e = check_tokens(d, q, k, v, alpha, beta, o)) != LQ_OK) return e;
     if ((e = check_ptr(b)) != LQ_OK) return e;
     lq::TokenPtrs t{q, k, v, alpha, beta, o, b};
     return hip_status(lq::launch_baseline(*d, S, state_dtype, t, (hipStream_t)stream));
@@ -222,7 +234,7 @@ const char *leapquant_strerror(int32_t status) {
     switch (status) {
         case LQ_OK: return "success";
         case LQ_EINVAL: return "invalid argument (NULL pointer, non-positive size or bad enum)";
-        case LQ_EALIGN: return "pointer not 16-byte aligned";
+        case LQ_EALIGN: return "pointer not aligned (16 bytes; 4 for beta and scalar-gate alpha)";
         case LQ_EUNSUPPORTED: return "unsupported shape or parameter (d_k/d_v must be 128, r <= 16, "
                                      "W within the gate's limit)";
         case LQ_EHIP: return "HIP runtime error (see leapquant_last_hip_error)";

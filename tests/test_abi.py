@@ -67,21 +67,30 @@ def test_validation_rejects_bad_arguments_before_launch():
     assert _call_decode(d, None, toks) == B.LQ_EINVAL
     assert _call_decode(d, st, [good, None, good, good, good, good]) == B.LQ_EINVAL
     assert _call_decode(d, st, [good, good + 4, good, good, good, good]) == B.LQ_EALIGN
+    # beta, and alpha under the scalar gate, need 4-byte alignment only (any tile
+    # count); a NULL output stops the call after those checks, before any launch
+    assert _call_decode(d, st, [good, good, good, good + 4, good + 4, None]) == B.LQ_EINVAL
+    assert _call_decode(d, st, [good, good, good, good, good + 2, None]) == B.LQ_EALIGN
+    dk = B.make_dims(2, 4, heads_k=2, gate=B.LQ_GATE_DIAG)
+    assert _call_decode(dk, st, [good, good, good, good + 4, good, None]) == B.LQ_EALIGN
     bad = B.lq_state(*([good] * 10))
     bad.rec_u = good + 2
     assert _call_decode(d, bad, toks) == B.LQ_EALIGN
     for kw, code in [({"d_k": 64}, B.LQ_EUNSUPPORTED), ({"n_comp": 17}, B.LQ_EUNSUPPORTED),
                      ({"window": 257}, B.LQ_EUNSUPPORTED), ({"window": 0}, B.LQ_EINVAL),
+                     ({"n_comp": -1}, B.LQ_EINVAL),
                      ({"gate": 2}, B.LQ_EINVAL), ({"code": 5}, B.LQ_EINVAL),
                      ({"n_comp": 2, "power_iters": 0}, B.LQ_EUNSUPPORTED),
                      ({"window": 65, "gate": B.LQ_GATE_DIAG}, B.LQ_EUNSUPPORTED)]:
         dd = B.make_dims(2, 4, heads_k=2, **kw)
         assert _call_decode(dd, st, toks) == code, kw
     assert _call_decode(B.make_dims(2, 4, heads_k=3), st, toks) == B.LQ_EINVAL
+    assert _call_decode(B.make_dims(0, 4, heads_k=2), st, toks) == B.LQ_EINVAL   # empty batch
     # size limits: batch * heads_v <= 2^30, and batch * heads_v * group < 2^32
     assert _call_decode(B.make_dims(1 << 26, 32, heads_k=32), st, toks) == B.LQ_EUNSUPPORTED
     assert _call_decode(B.make_dims(1 << 20, 256, heads_k=4), st, toks) == B.LQ_EUNSUPPORTED
-    assert _call_decode(B.make_dims(1 << 20, 256, heads_k=128), st, toks) != B.LQ_EUNSUPPORTED
+    # (a NULL output stops a call with valid dims before any launch)
+    assert _call_decode(B.make_dims(1 << 20, 256, heads_k=128), st, toks[:5] + [None]) == B.LQ_EINVAL
     L = B.lib()
     assert L.leapquant_baseline_step(C.byref(d), good, 7, *toks, None) == B.LQ_EINVAL
     assert L.leapquant_window_commit(C.byref(d), C.byref(st), good + 8, None) == B.LQ_EALIGN

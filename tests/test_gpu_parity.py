@@ -42,6 +42,11 @@ SMALL = {
     "w8_r16": W_["gdn_tiny"].with_(name="w8_r16", steps=64, window=8, n_comp=16),
     "w32_r4_nosmooth": W_["kda_kimi"].with_(name="w32_r4_nosmooth", batch=2, heads_v=4, heads_k=4,
                                             steps=64, window=32, n_comp=4, smooth=0, prefill=128),
+    # the largest window of the scalar gate (four record passes in the decode), and a
+    # ragged tile count (3 requests x 5 heads)
+    "gdn_w256": W_["gdn_tiny"].with_(name="gdn_w256", batch=2, heads_v=2, heads_k=2, steps=256, window=256,
+                                     prefill=128),
+    "ragged_3x5": W_["gdn_tiny"].with_(name="ragged_3x5", batch=3, heads_v=5, heads_k=5, steps=48, prefill=128),
     # b_t = 0 rows of the instance table: Mamba2 (scalar decay), GLA / RWKV6 (per-channel)
     "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1),
     "gla_small": W_["kda_kimi"].with_(name="gla_small", batch=2, heads_v=4, heads_k=4, steps=128,
