@@ -102,8 +102,9 @@ def _ptr(t):
     return t.data_ptr()
 
 
-def _need(t, nbytes: int, name: str):
-    """Marshalling check: a contiguous device tensor holding at least nbytes."""
+def _need(t, nbytes: int, name: str, dtype=None):
+    """Marshalling check: a contiguous device tensor (of `dtype`, if given)
+    holding at least nbytes.  Raw integer addresses are passed through."""
     if t is None:
         raise ValueError(f"{name} is required")
     if isinstance(t, int):
@@ -112,6 +113,8 @@ def _need(t, nbytes: int, name: str):
         raise ValueError(f"{name} must be a device tensor")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
     have = t.numel() * t.element_size()
     if have < nbytes:
         raise ValueError(f"{name} holds {have} bytes, the call needs {nbytes}")
@@ -127,16 +130,17 @@ def _check_state(dims, st):
 def _check_tokens(dims, q, k, v, alpha, beta, o):
     t, tk = dims.batch * dims.heads_v, dims.batch * dims.heads_k
     g = dims.d_k if dims.gate == LQ_GATE_DIAG else 1
-    _need(q, tk * dims.d_k * 4, "q")
-    _need(k, tk * dims.d_k * 4, "k")
-    _need(v, t * dims.d_v * 4, "v")
-    _need(alpha, t * g * 4, "alpha")
-    _need(beta, t * 4, "beta")
-    _need(o, t * dims.d_v * 4, "o")
+    f32 = torch.float32
+    _need(q, tk * dims.d_k * 4, "q", f32)
+    _need(k, tk * dims.d_k * 4, "k", f32)
+    _need(v, t * dims.d_v * 4, "v", f32)
+    _need(alpha, t * g * 4, "alpha", f32)
+    _need(beta, t * 4, "beta", f32)
+    _need(o, t * dims.d_v * 4, "o", f32)
 
 
 def _check_read(dims, b):
-    _need(b, dims.batch * dims.heads_v * dims.d_k * 4, "b")
+    _need(b, dims.batch * dims.heads_v * dims.d_k * 4, "b", torch.float32)
 
 
 def _stream(stream):
@@ -208,7 +212,7 @@ class State:
 
 def leapquant_quantize_state(dims: lq_dims, S: torch.Tensor, st: State, stream=None):
     _check_state(dims, st)
-    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * 4, "S")
+    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * 4, "S", torch.float32)
     s = st.struct()
     _check(_lib().leapquant_quantize_state(C.byref(dims), _ptr(S), C.byref(s), _stream(stream)),
            "leapquant_quantize_state")
@@ -249,7 +253,8 @@ def leapquant_window_commit(dims: lq_dims, st: State, mask=None, stream=None):
 def leapquant_baseline_step(dims: lq_dims, S, state_dtype: int, q, k, v, alpha, beta, o,
                             stream=None):
     width = 2 if state_dtype == LQ_STATE_BF16 else 4
-    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * width, "S")
+    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * width, "S",
+          torch.bfloat16 if state_dtype == LQ_STATE_BF16 else torch.float32)
     _check_tokens(dims, q, k, v, alpha, beta, o)
     _check(_lib().leapquant_baseline_step(C.byref(dims), _ptr(S), state_dtype, _ptr(q), _ptr(k),
                                           _ptr(v), _ptr(alpha), _ptr(beta), _ptr(o),
@@ -260,7 +265,8 @@ def leapquant_baseline_step(dims: lq_dims, S, state_dtype: int, q, k, v, alpha, 
 def leapquant_baseline_step_general(dims: lq_dims, S, state_dtype: int, q, k, b, v, alpha, beta, o,
                                     stream=None):
     width = 2 if state_dtype == LQ_STATE_BF16 else 4
-    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * width, "S")
+    _need(S, dims.batch * dims.heads_v * dims.d_v * dims.d_k * width, "S",
+          torch.bfloat16 if state_dtype == LQ_STATE_BF16 else torch.float32)
     _check_tokens(dims, q, k, v, alpha, beta, o)
     _check_read(dims, b)
     _check(_lib().leapquant_baseline_step_general(C.byref(dims), _ptr(S), state_dtype, _ptr(q),
@@ -271,7 +277,7 @@ def leapquant_baseline_step_general(dims: lq_dims, S, state_dtype: int, q, k, b,
 
 def leapquant_dequantize_state(dims: lq_dims, st: State, S_out, stream=None):
     _check_state(dims, st)
-    _need(S_out, dims.batch * dims.heads_v * dims.d_v * dims.d_k * 4, "S_out")
+    _need(S_out, dims.batch * dims.heads_v * dims.d_v * dims.d_k * 4, "S_out", torch.float32)
     s = st.struct()
     _check(_lib().leapquant_dequantize_state(C.byref(dims), C.byref(s), _ptr(S_out),
                                              _stream(stream)),
