@@ -250,8 +250,9 @@ def test_free_running_tiny():
 
 
 def test_partial_windows_mask_and_reset():
-    """Ragged schedule: tokens 0..20 then a commit of request 0 only, more tokens,
-    a commit of everything (partial windows), and a commit on empty windows."""
+    """Ragged schedule: 21 tokens, then a commit of request 0 only (a partial
+    window), a commit on its now-empty window (a no-op), and a commit of
+    everything (request 1's 21 records)."""
     wl = SMALL["kda_small"].with_(steps=40)
     cfg = H.ocfg(wl)
     S0 = H.oracle_prefill_state(wl)
@@ -310,6 +311,102 @@ def test_partial_windows_mask_and_reset():
     B.leapquant_window_commit(dims, st)     # all: request 1 commits its 21 records
     assert np.all(H.download_rep(st)["rec_len"] == 0)
     assert B.leapquant_check_error(st) == 0
+
+
+MIXED = {
+    "kda_mixed": (SMALL["kda_small"].with_(name="kda_mixed", batch=6, steps=64), [0, 1, 31, 32, 62, 63]),
+    "gqa_mixed": (SMALL["gqa_int8_small"].with_(name="gqa_mixed", batch=6, steps=64), [63, 0, 17, 48, 1, 62]),
+    # scalar gate at the largest window: positions in each of the decode's four record passes
+    "gdn_w256_mixed": (SMALL["gdn_w256"].with_(name="gdn_w256_mixed", batch=5), [0, 63, 64, 130, 255]),
+}
+
+
+@pytest.mark.parametrize("name", list(MIXED))
+def test_requests_at_different_window_positions_in_one_launch(name):
+    """A serving batch whose requests sit at different positions of their
+    windows: request b has n_b buffered records (the heads of a request share
+    its position, as grouped heads share q and k).  One decode launch must give
+    every tile the oracle's output for its own token n_b and append its record
+    at slot n_b, reading no slot at or past n_b (those hold NaN); a commit of
+    the resulting partial windows (p = n_b + 1 records, teacher-forced from the
+    oracle's records) must give the oracle's quantization of the reconstructed
+    state (Sec. 3.4 Eq. (smooth), Sec. 3.3)."""
+    wl, pos = MIXED[name]
+    W, Bn, Hv = wl.window, wl.batch, wl.heads_v
+    assert len(pos) == Bn and max(pos) < W
+    cfg = H.ocfg(wl)
+    dims = H.gdims(wl)
+    S0 = H.oracle_prefill_state(wl)
+    streams, tok = H.decode_tokens(wl, n=W)
+    otok = synth.tile_major(wl, streams, tok)
+    ref = O.run_dense(cfg, S0, otok, snapshots=True, history=True)
+    n_t = np.repeat(np.asarray(pos), Hv)                                 # position per tile
+    tiles = np.arange(wl.tiles)
+    start = [ref[k_][:, 0] for k_ in ("Z", "delta", "c", "Kt", "Ut")]
+    nan16 = torch.tensor(0x7E00, dtype=torch.int16, device="cuda")
+
+    def open_windows(st, n):
+        """Oracle records 0..n_t-1 per tile, NaN in every later slot, rec_len = n_t."""
+        H.upload_records(st, ref["hist_a"], ref["hist_k"], ref["hist_u"])
+        g = wl.dk if wl.gate == synth.GATE_DIAG else 1
+        ra = st.rec_a.view(wl.tiles, W, g).view(torch.int16)
+        rk = st.rec_k.view(wl.tiles, W, wl.dk).view(torch.int16)
+        ru = st.rec_u.view(wl.tiles, W, wl.dv).view(torch.int16)
+        past = torch.as_tensor(np.arange(W)[None, :] >= n[:, None], device="cuda")
+        for x in (ra, rk, ru):
+            x[past] = nan16
+        st.rec_len.view(-1)[:] = torch.as_tensor(n, dtype=torch.int32, device="cuda")
+
+    st = B.State.empty(dims)
+    H.upload_rep(st, tiles, *start)
+    open_windows(st, n_t)
+    # the launch: request b takes token pos[b] of its own stream
+    sm = synth.step_major_full(wl, tok)
+    rq = np.arange(Bn)
+    args = [H.dev(np.ascontiguousarray(sm[f][np.asarray(pos), rq])) for f in ("q", "k", "v", "alpha", "beta")]
+    o = torch.empty((Bn, Hv, wl.dv), dtype=torch.float32, device="cuda")
+    B.leapquant_decode_step(dims, st, *args, o)
+    og = o.view(wl.tiles, wl.dv).cpu().numpy()
+    exp_o = ref["o"][tiles, n_t]
+    o_rel = H.rel_rows(og[:, None], exp_o[:, None])
+    g = wl.dk if wl.gate == synth.GATE_DIAG else 1
+    got_len = st.rec_len.view(-1).cpu().numpy()
+    rk = st.rec_k.view(wl.tiles, W, wl.dk)[tiles, n_t].cpu().numpy().view(np.uint16)
+    ru = st.rec_u.view(wl.tiles, W, wl.dv)[tiles, n_t].cpu().numpy().view(np.uint16)
+    ra = st.rec_a.view(wl.tiles, W, g)[tiles, n_t].cpu().numpy().view(np.uint16)
+    ek = H.f16_bits(ref["hist_k"][tiles, n_t])
+    eu = H.f16_bits(ref["hist_u"][tiles, n_t])
+    ea = H.f16_bits(ref["hist_a"][tiles, n_t])
+    u_rel = H.rel_rows(H.f16_vals(ru)[:, None], ref["hist_u"][tiles, n_t][:, None])
+    H.log(f"[{name}] o_rel {o_rel:.3e} u_rel {u_rel:.3e} k_eq {np.mean(rk == ek):.5f} "
+          f"u_eq {np.mean(ru == eu):.5f}")
+    assert B.leapquant_check_error(st) == 0
+    assert np.array_equal(got_len, n_t + 1)
+    assert np.all(np.isfinite(og)) and o_rel <= 1e-3
+    assert np.array_equal(ra, ea)
+    assert np.mean(rk == ek) >= 0.999 and int(H._f16_ulp_dist(rk, ek).max()) <= 1
+    assert np.mean(ru == eu) >= 0.995 and u_rel <= 1e-3
+    # commit of the partial windows, from the oracle's records
+    p_t = n_t + 1
+    st2 = B.State.empty(dims)
+    H.upload_rep(st2, tiles, *start)
+    open_windows(st2, p_t)
+    B.leapquant_window_commit(dims, st2)
+    got = H.download_rep(st2)
+    assert np.all(got["rec_len"] == 0) and B.leapquant_check_error(st2) == 0
+    exp = {k_: [] for k_ in ("Z", "delta", "c", "Kt", "Ut")}
+    for i in tiles:
+        rep0 = O.Rep(*(x[i] for x in start))
+        p = int(p_t[i])
+        Sp = O.reconstruct(cfg, rep0, None, ref["hist_a"][i, :p], ref["hist_k"][i, :p], ref["hist_u"][i, :p])
+        rp = O.quantize(cfg, Sp)
+        for k_ in exp:
+            exp[k_].append(getattr(rp, k_))
+    exp = {k_: np.stack(v_) for k_, v_ in exp.items()}
+    cr = H.compare_rep(cfg, {k_: got[k_] for k_ in exp}, exp, wl.code)
+    H.log(f"[{name}] partial-window commit {cr}")
+    assert cr["code_eq"] >= 0.999 and cr["code_maxdiff"] <= 1 and cr["deq_rel"] <= 1e-3, cr
+    assert cr.get("comp_rel", 0.0) <= 1e-3 and cr["delta_rel"] <= 1e-5 and cr["c_rel"] <= 1e-5, cr
 
 
 def test_full_window_raises_device_error_and_leaves_state():
