@@ -375,9 +375,8 @@ def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3):
     o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
 
     def sub(b0, b1):
-        d = B_.make_dims(b1 - b0, wl.heads_v, wl.heads_k, window=W, n_comp=wl.n_comp,
-                         power_iters=wl.power_iters, gate=wl.gate, code=wl.code)
-        return d, B_.State(d, *[getattr(st, f)[b0:b1] if f != "err" else st.err for f in B_.FIELDS])
+        v = st.requests(b0, b1)
+        return v.dims, v
 
     res = {}
     for G in groups:

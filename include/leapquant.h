@@ -16,9 +16,12 @@
  *  - One tile = one (request b, value head h) pair; tiles are numbered
  *    b * heads_v + h.  d_k = d_v = 128 in this version.
  *  - Every array argument is a caller-owned DEVICE pointer, dense, row-major,
- *    16-byte aligned, except the per-tile scalars beta and (scalar gate) alpha,
- *    which need 4-byte alignment only (so one step of a step-major buffer can
- *    be passed for any tile count).  The library allocates no memory, keeps no global state
+ *    16-byte aligned, except the arrays read one element at a time: the
+ *    per-tile scalars beta and (scalar gate) alpha, rec_len, err and the
+ *    commit mask need 4-byte alignment, the scalar gate's rec_a 2-byte
+ *    alignment.  So one step of a step-major token buffer, or a state whose
+ *    arrays all start at the same tile of a larger one (a group of requests),
+ *    can be passed for any tile count.  The library allocates no memory, keeps no global state
  *    and never synchronises (except leapquant_check_error).  Work is enqueued on
  *    `stream` (a hipStream_t; NULL = the default stream) and returns at once.
  *    Calls on different streams with disjoint buffers may run concurrently.
@@ -46,7 +49,7 @@ extern "C" {
 /* ---- status codes ---- */
 #define LQ_OK            0
 #define LQ_EINVAL       -1   /* NULL pointer, non-positive size, inconsistent heads   */
-#define LQ_EALIGN       -2   /* a pointer is not aligned (16 bytes; 4 for beta / alpha) */
+#define LQ_EALIGN       -2   /* a pointer is not aligned as its array requires     */
 #define LQ_EUNSUPPORTED -3   /* d_k/d_v != 128, r > 16, W out of range, ...           */
 #define LQ_EHIP         -4   /* a HIP call failed (kernel launch, synchronisation)    */
 #define LQ_EDEVICE      -5   /* a sticky device error was found by check_error        */

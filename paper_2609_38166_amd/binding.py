@@ -206,6 +206,16 @@ class State:
     def struct(self) -> lq_state:
         return lq_state(*[getattr(self, f).data_ptr() for f in FIELDS])
 
+    def requests(self, b0: int, b1: int) -> "State":
+        """Requests b0 .. b1-1 as views into this state (every array starts at
+        tile b0 * heads_v; the error word is shared), with dims for b1 - b0
+        requests: a group that runs on its own schedule or stream."""
+        if not 0 <= b0 < b1 <= self.dims.batch:
+            raise ValueError(f"request range [{b0}, {b1}) outside [0, {self.dims.batch})")
+        d = lq_dims.from_buffer_copy(self.dims)
+        d.batch = b1 - b0
+        return State(d, *[self.err if f == "err" else getattr(self, f)[b0:b1] for f in FIELDS])
+
     def nbytes(self) -> int:
         return sum(getattr(self, f).numel() * getattr(self, f).element_size() for f in FIELDS)
 

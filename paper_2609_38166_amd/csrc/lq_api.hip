@@ -55,28 +55,32 @@ int32_t check_dims(const lq_dims *d) {
     return LQ_OK;
 }
 
+// Arrays that every kernel reads one element at a time need only the
+// element's alignment: the per-tile scalars beta and (scalar gate) alpha,
+// rec_len, err and the commit mask 4 bytes, the scalar gate's FP16 decays
+// 2 bytes.  So step-major token buffers can be passed one step at a time, and
+// a group of requests as views into a larger state, for any tile count.  Every
+// other array is read in 16-byte vectors by some kernel.
+int32_t check_ptr_n(const void *p, uintptr_t n) {
+    if (!p) return LQ_EINVAL;
+    if ((uintptr_t)p & (n - 1)) return LQ_EALIGN;
+    return LQ_OK;
+}
+int32_t check_ptr4(const void *p) { return check_ptr_n(p, 4); }
+
 int32_t check_state(const lq_dims *d, const lq_state *st) {
     if (!st) return LQ_EINVAL;
     int32_t e;
-    const void *ptrs[] = {st->codes, st->scale, st->smooth, st->rec_k, st->rec_u, st->rec_a,
-                          st->rec_len};
+    const void *ptrs[] = {st->codes, st->scale, st->smooth, st->rec_k, st->rec_u};
     for (const void *p : ptrs)
         if ((e = check_ptr(p)) != LQ_OK) return e;
+    if ((e = d->gate == LQ_GATE_DIAG ? check_ptr(st->rec_a) : check_ptr_n(st->rec_a, 2)) != LQ_OK) return e;
+    if ((e = check_ptr4(st->rec_len)) != LQ_OK) return e;
     if (d->n_comp > 0) {
         if ((e = check_ptr(st->comp_k)) != LQ_OK) return e;
         if ((e = check_ptr(st->comp_u)) != LQ_OK) return e;
     }
-    if ((e = check_ptr(st->err)) != LQ_OK) return e;
-    return LQ_OK;
-}
-
-// Per-tile scalar arrays (beta, and alpha under the scalar gate) are read one
-// word at a time and need only 4-byte alignment, so that step-major buffers of
-// any tile count can be passed one step at a time; every other array is read
-// in 16-byte vectors by some kernel.
-int32_t check_ptr4(const void *p) {
-    if (!p) return LQ_EINVAL;
-    if ((uintptr_t)p & 3u) return LQ_EALIGN;
+    if ((e = check_ptr4(st->err)) != LQ_OK) return e;
     return LQ_OK;
 }
 
@@ -169,7 +173,7 @@ int32_t leapquant_window_commit(const lq_dims *d, lq_state *st, const int32_t *m
     int32_t e = check_dims(d);
     if (e != LQ_OK) return e;
     if ((e = check_state(d, st)) != LQ_OK) return e;
-    if (mask && !aligned(mask)) return LQ_EALIGN;
+    if (mask && ((uintptr_t)mask & 3u)) return LQ_EALIGN;
     return hip_status(lq::launch_tile(*d, state_ptrs(st), lq::TILE_COMMIT, nullptr, nullptr, mask,
                                       (hipStream_t)stream));
 }
@@ -234,7 +238,8 @@ const char *leapquant_strerror(int32_t status) {
     switch (status) {
         case LQ_OK: return "success";
         case LQ_EINVAL: return "invalid argument (NULL pointer, non-positive size or bad enum)";
-        case LQ_EALIGN: return "pointer not aligned (16 bytes; 4 for beta and scalar-gate alpha)";
+        case LQ_EALIGN: return "pointer not aligned (16 bytes; 4 for beta, scalar-gate alpha, rec_len, err "
+                               "and mask; 2 for scalar-gate rec_a)";
         case LQ_EUNSUPPORTED: return "unsupported shape or parameter (d_k/d_v must be 128, r <= 16, "
                                      "W within the gate's limit)";
         case LQ_EHIP: return "HIP runtime error (see leapquant_last_hip_error)";

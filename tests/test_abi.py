@@ -76,6 +76,20 @@ def test_validation_rejects_bad_arguments_before_launch():
     bad = B.lq_state(*([good] * 10))
     bad.rec_u = good + 2
     assert _call_decode(d, bad, toks) == B.LQ_EALIGN
+    # rec_len, err and the scalar gate's rec_a are read one element at a time:
+    # views of a group of requests inside a larger state pass for any tile offset
+    # (a NULL output stops each call after the state checks)
+    no_out = toks[:5] + [None]
+    for field, off, code in [("rec_len", 4, B.LQ_EINVAL), ("rec_len", 2, B.LQ_EALIGN),
+                             ("err", 4, B.LQ_EINVAL), ("err", 2, B.LQ_EALIGN),
+                             ("rec_a", 2, B.LQ_EINVAL), ("rec_a", 1, B.LQ_EALIGN),
+                             ("codes", 4, B.LQ_EALIGN), ("scale", 8, B.LQ_EALIGN)]:
+        v = B.lq_state(*([good] * 10))
+        setattr(v, field, good + off)
+        assert _call_decode(d, v, no_out) == code, (field, off)
+    v = B.lq_state(*([good] * 10))
+    v.rec_a = good + 2                   # the diagonal gate reads 16-byte decay vectors
+    assert _call_decode(dk, v, no_out) == B.LQ_EALIGN
     for kw, code in [({"d_k": 64}, B.LQ_EUNSUPPORTED), ({"n_comp": 17}, B.LQ_EUNSUPPORTED),
                      ({"window": 257}, B.LQ_EUNSUPPORTED), ({"window": 0}, B.LQ_EINVAL),
                      ({"n_comp": -1}, B.LQ_EINVAL),
@@ -93,7 +107,7 @@ def test_validation_rejects_bad_arguments_before_launch():
     assert _call_decode(B.make_dims(1 << 20, 256, heads_k=128), st, toks[:5] + [None]) == B.LQ_EINVAL
     L = B.lib()
     assert L.leapquant_baseline_step(C.byref(d), good, 7, *toks, None) == B.LQ_EINVAL
-    assert L.leapquant_window_commit(C.byref(d), C.byref(st), good + 8, None) == B.LQ_EALIGN
+    assert L.leapquant_window_commit(C.byref(d), C.byref(st), good + 2, None) == B.LQ_EALIGN   # mask: 4 bytes
     assert L.leapquant_quantize_state(C.byref(d), None, C.byref(st), None) == B.LQ_EINVAL
     assert L.leapquant_dequantize_state(C.byref(d), C.byref(st), good + 1, None) == B.LQ_EALIGN
     assert L.leapquant_check_error(None, None, None) == B.LQ_EINVAL

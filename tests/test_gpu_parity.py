@@ -409,6 +409,56 @@ def test_requests_at_different_window_positions_in_one_launch(name):
     assert cr.get("comp_rel", 0.0) <= 1e-3 and cr["delta_rel"] <= 1e-5 and cr["c_rel"] <= 1e-5, cr
 
 
+VIEWS = {
+    # 3 requests x 5 heads at W = 21: the group starting at request 1 puts rec_len
+    # 20 bytes and the scalar gate's rec_a 210 bytes into their arrays
+    "gdn_groups": SMALL["ragged_3x5"].with_(name="gdn_groups", window=21, steps=30),
+    "kda_groups": SMALL["kda_small"].with_(name="kda_groups", batch=3, heads_v=5, heads_k=5, window=16,
+                                           steps=24, n_comp=4, prefill=128),
+}
+
+
+@pytest.mark.parametrize("name", list(VIEWS))
+def test_request_groups_as_state_views(name):
+    """Requests split into groups [0, 1) and [1, 3), each run through views into
+    the whole state (State.requests) on a stream of its own: decode outputs and
+    the state after a full window's commit and a partial window are
+    bit-identical to whole-batch calls."""
+    wl = VIEWS[name]
+    dims = H.gdims(wl)
+    S = H.oracle_prefill_state(wl)
+    _, tok = H.decode_tokens(wl)
+    dt = H.DeviceTokens(wl, tok)
+    whole = B.State.empty(dims)
+    B.leapquant_quantize_state(dims, H.dev(S.transpose(0, 2, 1).astype(np.float32)), whole)
+    grouped = B.State(dims, *[getattr(whole, f).clone() for f in B.FIELDS])
+    groups = [(0, 1), (1, 3)]
+    views = [grouped.requests(b0, b1) for b0, b1 in groups]
+    streams = [torch.cuda.Stream() for _ in groups]
+    o_whole = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+    o_grp = torch.empty_like(o_whole)
+    main = torch.cuda.current_stream()
+    for t in range(wl.steps):
+        B.leapquant_decode_step(dims, whole, *dt.step(t), o_whole)
+        for s_ in streams:
+            s_.wait_stream(main)
+        for (b0, b1), v, s_ in zip(groups, views, streams):
+            x = [a[b0:b1] for a in dt.step(t)]
+            B.leapquant_decode_step(v.dims, v, *x, o_grp[b0:b1], stream=s_)
+            if (t + 1) % wl.window == 0:
+                B.leapquant_window_commit(v.dims, v, stream=s_)
+        for s_ in streams:
+            main.wait_stream(s_)
+        if (t + 1) % wl.window == 0:
+            B.leapquant_window_commit(dims, whole)
+        assert torch.equal(o_grp, o_whole), t
+    torch.cuda.synchronize()
+    for f in B.FIELDS:
+        assert torch.equal(getattr(grouped, f), getattr(whole, f)), f
+    assert int(whole.rec_len[0, 0]) == wl.steps % wl.window
+    assert B.leapquant_check_error(grouped) == 0
+
+
 def test_full_window_raises_device_error_and_leaves_state():
     wl = SMALL["gdn_tiny"].with_(window=2, steps=3)
     dims = H.gdims(wl)
