@@ -361,12 +361,15 @@ def decode_two_batches(wl, dims, S0, toks, reps=3):
     return float(np.mean(ts))
 
 
-def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3):
+def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3, one_batch=False):
     """Average time per decode step over one window cycle (W steps, one commit
     per request) when the requests are split into G groups whose windows are
-    offset by W/G steps, each group on its own stream (its commit follows its
-    own decode; the other groups' decodes can run beside it), replayed as one
-    graph.  G = 1 is the aligned schedule of the headline step."""
+    offset by W/G steps, replayed as one graph.  Each group runs on its own
+    stream (its commit follows its own decode; the other groups' decodes can
+    run beside it), or with one_batch every step is one decode launch over all
+    requests at their mixed window positions, followed by a commit masked to
+    the group whose window just ended.  G = 1 is the aligned schedule of the
+    headline step."""
     import torch
     from paper_2609_38166_amd import binding as B_
     W, Bt = wl.window, wl.batch
@@ -383,8 +386,20 @@ def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3):
         R = Bt // G
         parts = [(gi * R, (gi + 1) * R, (gi * W // G) % W) + sub(gi * R, (gi + 1) * R) for gi in range(G)]
         streams = [torch.cuda.Stream() for _ in range(G)]
+        masks = []
+        for b0, b1, _, _, _ in parts:
+            mk = torch.zeros(Bt, dtype=torch.int32, device="cuda")
+            mk[b0:b1] = 1
+            masks.append(mk)
 
-        def cycle():
+        def cycle_one_batch():
+            for t in range(W):
+                B_.leapquant_decode_step(dims, st, q[t], k[t], v[t], a[t], b[t], o)
+                for (b0, b1, off, _, _), mk in zip(parts, masks):
+                    if (t + 1 + off) % W == 0:
+                        B_.leapquant_window_commit(dims, st, mk)
+
+        def cycle_streams():
             main = torch.cuda.current_stream()
             for s_ in streams:
                 s_.wait_stream(main)
@@ -397,6 +412,8 @@ def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3):
                             B_.leapquant_window_commit(d, sv)
             for s_ in streams:
                 main.wait_stream(s_)
+
+        cycle = cycle_one_batch if one_batch else cycle_streams
 
         def reset():
             B_.leapquant_quantize_state(dims, S0, st)
@@ -424,7 +441,7 @@ def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3):
                 ts.append(e0.elapsed_time(e1) / W)
         if B_.leapquant_check_error(st):
             raise RuntimeError("device error during the staggered-window timing")
-        res[f"G{G}_us_per_step"] = round(float(np.mean(ts)) * 1e3, 2)
+        res[f"G{G}{'_one_batch' if one_batch else ''}_us_per_step"] = round(float(np.mean(ts)) * 1e3, 2)
         del g
     del st
     return res
@@ -662,8 +679,11 @@ def main():
     log(f"[bench] decode with two alternating batches {two * 1e3:.1f} us/launch")
     if not args.no_variants:
         out["staggered_windows"] = staggered_windows(wl, dims, S0, toks)
+        out["staggered_windows"].update(staggered_windows(wl, dims, S0, toks, groups=(4,), one_batch=True))
         out["staggered_windows"]["note"] = ("requests in G groups whose windows are offset by W/G, one stream "
-                                            "per group; per decode step over one window cycle incl. commits")
+                                            "per group (one_batch: one decode launch over the mixed window "
+                                            "positions, then a commit masked to the group whose window ended); "
+                                            "per decode step over one window cycle incl. commits")
         log(f"[bench] staggered windows {out['staggered_windows']}")
     ceil = stream_read_ceiling()
     out["stream_read_ceiling"] = ceil
