@@ -312,6 +312,42 @@ def rwkv7_tokens(wl, n_sub, seed):
     return tuple(t_.contiguous() for t_ in toks)
 
 
+def bulk_quantize(reps=3):
+    """leapquant_quantize_state over the bulk prefix-cache workload: 8192
+    cached requests x 32 heads (262144 fp32 states, 17.2 GB resident in HBM),
+    r = 8.  Returns ms per pass and GB/s of fp32 state read.  The states are
+    drawn on the device (N(0, 1)); the kernel's work does not depend on the
+    values."""
+    import torch
+    from paper_2609_38166_amd import binding as B_, synth
+    wl = synth.WORKLOADS["bulk_quantize"]
+    dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=wl.window, n_comp=wl.n_comp,
+                        power_iters=wl.power_iters, gate=wl.gate, code=wl.code)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(wl.seed)
+    S = torch.randn((wl.batch, wl.heads_v, wl.dv, wl.dk), dtype=torch.float32, device="cuda", generator=g)
+    st = B_.State.empty(dims)
+    B_.leapquant_quantize_state(dims, S, st)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        B_.leapquant_quantize_state(dims, S, st)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    if B_.leapquant_check_error(st):
+        raise RuntimeError("device error during the bulk quantization")
+    ms = float(np.median(ts))
+    nbytes = S.numel() * 4
+    del S, st
+    torch.cuda.empty_cache()
+    return {"states": wl.tiles, "ms": round(ms, 3), "gbps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "fp32_bytes": nbytes, "n_comp": wl.n_comp,
+            "note": "fp64 fit, smoothing and codes per state: bound by vector-ALU issue, not by HBM"}
+
+
 def decode_two_batches(wl, dims, S0, toks, reps=3):
     """Average decode launch duration when two independent batches of the same
     size alternate launch by launch (positions 1..W each, one graph): the other
@@ -678,6 +714,8 @@ def main():
         "note": "two batches alternate, so no batch's codes stay in the Infinity Cache between its steps"}
     log(f"[bench] decode with two alternating batches {two * 1e3:.1f} us/launch")
     if not args.no_variants:
+        out["bulk_quantize"] = bulk_quantize()
+        log(f"[bench] bulk quantize {out['bulk_quantize']}")
         out["staggered_windows"] = staggered_windows(wl, dims, S0, toks)
         out["staggered_windows"].update(staggered_windows(wl, dims, S0, toks, groups=(4,), one_batch=True))
         out["staggered_windows"]["note"] = ("requests in G groups whose windows are offset by W/G, one stream "

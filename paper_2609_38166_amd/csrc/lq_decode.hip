@@ -86,19 +86,6 @@ struct RecRegs {
     uint32_t as[PER_SLOT];           // FP16 decay (scalar gate), converted where used
 };
 
-// LDS byte address of a __shared__ object.
-__device__ __forceinline__ uint32_t lds_addr(const void *p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
-}
-
-// Copy 16 bytes per lane from global memory straight into LDS: lane L of the
-// wave writes lds_base + 16 L (lds_base uniform).  Issued from asm so that the
-// compiler does not treat it as an LDS store that every later LDS access must
-// wait for; the reader waits with wait_vm_all() and a barrier.  This kernel
-// uses M0 for nothing else.
-__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(g), "s"(lds_base) : "memory");
-}
 
 // Non-temporal 16-byte load, for the records: a step streams every tile's
 // buffered records once, and as plain loads they would evict the codes from
@@ -109,7 +96,6 @@ __device__ __forceinline__ uint4 ld_stream16(const uint16_t *p) {
     const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
     return make_uint4(v.x, v.y, v.z, v.w);
 }
-__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Sum of x over the 4 slots (16-lane rows) of a wave, for 8 values per lane,
 // as a reduce-scatter: lane (row rho, l16) returns the sums of values 2 rho

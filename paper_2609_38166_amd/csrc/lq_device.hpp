@@ -206,4 +206,20 @@ __device__ __forceinline__ uint2 encode8(const uint32_t *c) {
 template <typename T>
 __device__ __forceinline__ T ld(const T *p) { return *p; }
 
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// Copy 16 bytes per lane from global memory straight into LDS: lane L of the
+// wave writes lds_base + 16 L (lds_base uniform).  Issued from asm so that the
+// compiler does not treat it as an LDS store that every later LDS access must
+// wait for; the reader waits with wait_vm_all() and a barrier.  M0 is set here
+// and not declared clobbered (the compiler reserves it): the kernels that call
+// this use M0 for nothing else, which their generated code shows.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(g), "s"(lds_base) : "memory");
+}
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 }  // namespace lq

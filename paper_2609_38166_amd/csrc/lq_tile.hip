@@ -3,8 +3,12 @@
 // One 256-thread workgroup (4 waves) owns one 128 x 128 tile held in
 // registers: thread (kb, vb) keeps the 8 x 8 block M[8kb .. 8kb+7][8vb .. 8vb+7]
 // of the state in paper orientation (row = key channel).  kb is the lane's
-// column inside its 16-lane DPP row, so reductions over key channels are DPP
-// row reductions; reductions over value channels go through LDS.
+// column inside its 16-lane DPP row, so sums over key channels stay inside a
+// wave; sums over value channels go through LDS.  Three workgroups share a CU
+// (168 VGPRs per lane, 50 KiB of LDS each): the 128 registers of the fp64
+// block leave 40 for everything else, so the code below keeps few values
+// live across phases (lane coordinates re-derived where used, records kept
+// packed, the next pass's records copied straight into LDS).
 //
 //   commit   : reconstruct S_p = Gamma_{1:p}[C dequant(Z) + K~ U~^T]
 //              + sum_j Gamma_{j+1:p} k~_j u_j^T  (Sec. 3.4 Eq. (smooth)),
@@ -16,8 +20,8 @@
 // Quantization (Sec. 3.3 Eq. (compensator-rank-r), Sec. 3.4, App. B.3): r
 // Compensator Tokens fitted one after another by power iteration on the
 // deflated residual (start: key-row l2 norms; each sweep y = M^T x, x = M y;
-// the direction is normalised), each rounded to FP16 before it is subtracted; then the smoothing
-// scales c_k = sqrt(max(mean_v |R_kv|, 1e-12)), the per-value-channel scale
+// the direction is normalised), each rounded to FP16 before it is
+// subtracted; then the smoothing scales c_k = sqrt(max(mean_v |R_kv|, 1e-12)), the per-value-channel scale
 // delta_v = max_k |R_kv / c_k| / qmax and the codes.
 //
 // Precision: the tile, the fit and the smoothing statistic are carried in
@@ -113,41 +117,43 @@ struct TileShared {
     };
 };
 
-// Sum p[a] (channel 8kb+a, this thread's value block) over the 16 value
-// blocks through LDS; thread t < 128 returns the sum for channel KCH(t).
-__device__ __forceinline__ double reduce_over_values(TileShared &sh, const double *p, int kb, int vb) {
-#pragma unroll
-    for (int a = 0; a < 8; ++a) sh.part[vb][KP(kb, a)] = p[a];
+// Sums over value channels in two halves: each thread stores its value
+// block's partial for channel 8kb+a as soon as it has it (put_part), then
+// sum_parts adds the 16 value blocks; thread t < 128 gets channel KCH(t).
+__device__ __forceinline__ void put_part(TileShared &sh, int a, double p, int kb, int vb) {
+    sh.part[vb][KP(kb, a)] = p;
+}
+__device__ __forceinline__ double sum_parts(TileShared &sh) {
     __syncthreads();
     double s = 0.0;
     const int t = threadIdx.x;
     if (t < D) {
-        double v[NVB];
+        double v[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int j = 0; j < NVB; ++j) v[j] = sh.part[j][t];
-#pragma unroll
-        for (int w = NVB / 2; w >= 1; w /= 2)
-#pragma unroll
-            for (int j = 0; j < w; ++j) v[j] += v[j + w];
-        s = v[0];
+        for (int j = 0; j < NVB; ++j) v[j & 3] += sh.part[j][t];
+        s = (v[0] + v[1]) + (v[2] + v[3]);
     }
     return s;
 }
 
-// Threads t < 128 publish x (channel KCH(t)); after the barrier every thread reads
-// its 8 channels into xa and gets the squared norm of the whole vector.  The
-// barrier also ends every read of sh.part issued before the call.
-__device__ __forceinline__ double publish_vector(TileShared &sh, double x, double *xa, int kb) {
+// Threads t < 128 publish x (channel KCH(t)) to sh.vec, which every thread
+// then reads where it needs it (channel 8kb+a at KP(kb, a)); with_norm also
+// returns the squared norm of the whole vector.  The barrier also ends every
+// read of sh.part issued before the call.
+__device__ __forceinline__ double publish(TileShared &sh, double x, bool with_norm) {
     const int t = threadIdx.x;
     if (t < D) {
         sh.vec[t] = x;
-        const double s = wave_sum(x * x);
-        if ((t & 63) == 0) sh.nrm[t >> 6] = s;
+        if (with_norm) {
+            const double s = wave_sum(x * x);
+            if ((t & 63) == 0) sh.nrm[t >> 6] = s;
+        }
     }
     __syncthreads();
-#pragma unroll
-    for (int a = 0; a < 8; ++a) xa[a] = sh.vec[KP(kb, a)];
-    return sh.nrm[0] + sh.nrm[1];
+    if (!with_norm) return 0.0;
+    int z = 0;                           // a zero made where it is used (not held across the fit)
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    return sh.nrm[z] + sh.nrm[z + 1];
 }
 
 // Sum v[b] (b = 0..7, this thread's value channels) over the 16 key blocks
@@ -163,37 +169,32 @@ __device__ __forceinline__ void row_sum8(TileShared &sh, double *v, int kb, int 
     for (int b = 0; b < 8; ++b) r[17 * b + kb] = v[b];
     __builtin_amdgcn_wave_barrier();
     const int c = kb & 7;
-    double t[16];
+    double t[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int l = 0; l < 16; ++l) t[l] = r[17 * c + l];
-#pragma unroll
-    for (int w = 8; w >= 1; w /= 2)
-#pragma unroll
-        for (int l = 0; l < w; ++l) t[l] += t[l + w];
-    if (kb < 8) r[17 * c + 16] = t[0] * scale;
+    for (int l = 0; l < 16; ++l) t[l & 3] += r[17 * c + l];
+    if (kb < 8) r[17 * c + 16] = ((t[0] + t[1]) + (t[2] + t[3])) * scale;
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int b = 0; b < 8; ++b) v[b] = r[17 * b + 16];
     __builtin_amdgcn_wave_barrier();
 }
 
-// publish_vector without the norm.
-__device__ __forceinline__ void publish_only(TileShared &sh, double x, double *xa, int kb) {
-    const int t = threadIdx.x;
-    if (t < D) sh.vec[t] = x;
-    __syncthreads();
-#pragma unroll
-    for (int a = 0; a < 8; ++a) xa[a] = sh.vec[KP(kb, a)];
-}
-
 template <int GATE, int CODE, int MODE>
-__global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
+__global__ __launch_bounds__(TT, 3) void tile_kernel(TileArgs A) {
     __shared__ TileShared sh;
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int kb = lane & 15;                       // key block of 8 channels (DPP column)
-    const int vb = tid >> 4;                        // value block of VPT channels (0..15)
+    int kb = tid & 15;                              // key block of 8 channels (DPP column)
+    int vb = tid >> 4;                              // value block of VPT channels (0..15)
+    // re-derive the lane coordinates from an opaque thread index, so that the
+    // compiler recomputes the addresses built from them instead of holding
+    // them in registers across phases
+    auto refresh = [&]() {
+        int t = (int)threadIdx.x;
+        asm volatile("" : "+v"(t));
+        kb = t & 15;
+        vb = t >> 4;
+    };
     const size_t tvec = (size_t)tile * D;
     const int r = A.n_comp;
 
@@ -238,14 +239,30 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
         // records in passes of TCH, oldest pass first; slot ts of a pass takes
         // record lo+ts, lane l16 its 8-channel / 8-value segment.
         const size_t rbase = (size_t)tile * A.window;
-        uint4 rk = make_uint4(0, 0, 0, 0), ru = rk, ra = rk;
+        // the tile's record arrays as uniform bases, the lane's part as a 32-bit
+        // offset (no per-lane 64-bit address is held across the passes)
+        const uint16_t *rkb = A.rec_k + rbase * D, *rub = A.rec_u + rbase * D;
+        const uint16_t *rab = A.rec_a + rbase * (GATE ? D : 1);
+        // A pass's records are copied straight into LDS (the raw FP16 words,
+        // in the record-staging area, which is idle while the previous pass's
+        // records are applied), so no register holds them across a pass;
+        // wave w copies records lo + 4w .. lo + 4w + 3.  The scalar gate's one
+        // decay per record is loaded into a register.
+        uint4 (*raw)[TCH][16] = (uint4 (*)[TCH][16])sh.pre;   // [key, corr, decay][record][segment]
+        uint32_t ras = 0;
         auto load_pass = [&](int lo_, int hi_) {
-            const int rr = lo_ + ts;
+            const int t = (int)threadIdx.x;
+            const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+            const int rr = lo_ + 4 * w + ((t & 63) >> 4);
+            const uint32_t off = (uint32_t)rr * D + 8u * (t & 15);
             if (rr < hi_) {
-                rk = *(const uint4 *)(A.rec_k + (rbase + rr) * D + 8 * l16);
-                ru = *(const uint4 *)(A.rec_u + (rbase + rr) * D + 8 * l16);
-                if (GATE) ra = *(const uint4 *)(A.rec_a + (rbase + rr) * D + 8 * l16);
-                else ra.x = A.rec_a[rbase + rr];
+                dma16(rkb + off, lds_addr(&raw[0][4 * w][0]));
+                dma16(rub + off, lds_addr(&raw[1][4 * w][0]));
+                if (GATE) dma16(rab + off, lds_addr(&raw[2][4 * w][0]));
+            }
+            if (!GATE) {
+                const int rs = lo_ + (t >> 4);
+                if (rs < hi_) ras = rab[rs];
             }
         };
         if (p > 0) load_pass(0, p < TCH ? p : TCH);
@@ -255,10 +272,10 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
             const float dv[8] = {dl0.x, dl0.y, dl0.z, dl0.w, dl1.x, dl1.y, dl1.z, dl1.w};
             const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
 #pragma unroll
-            for (int a = 0; a < 8; ++a) {
+            for (int b = 0; b < VPT; ++b) {
+                const uint32_t w[2] = {zp[b].x, zp[b].y};
 #pragma unroll
-                for (int b = 0; b < VPT; ++b) {
-                    const uint32_t w[2] = {zp[b].x, zp[b].y};
+                for (int a = 0; a < 8; ++a) {
                     const double zf = (double)code_at<CODE>(w, a);
                     m[a][b] = (double)cv[a] * (zf * (double)dv[b]);
                 }
@@ -278,55 +295,72 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
         __syncthreads();
 #pragma unroll 1
         for (int h = 0; h < r; ++h) {
-            double kd[8], ud[VPT];
-#pragma unroll
-            for (int a = 0; a < 8; ++a) kd[a] = sh.key[h][KP(kb, a)];
+            refresh();
+            double ud[VPT];
 #pragma unroll
             for (int b = 0; b < VPT; ++b) ud[b] = (double)sh.val[h][VPT * vb + b];
 #pragma unroll
-            for (int a = 0; a < 8; ++a)
+            for (int a = 0; a < 8; ++a) {
+                const double kd = sh.key[h][KP(kb, a)];
 #pragma unroll
-                for (int b = 0; b < VPT; ++b) m[a][b] = fma(kd[a], ud[b], m[a][b]);
+                for (int b = 0; b < VPT; ++b) m[a][b] = fma(kd, ud[b], m[a][b]);
+            }
         }
+        wait_vm_all();          // the first pass's records have landed in LDS
         __syncthreads();
 
         // Each pass: m <- Gamma_pass * m + sum_j Gamma_{j+1:hi} k~_j u_j^T, the
         // window recursion taken TCH records at a time; within the pass the
         // decay of every later record is an exclusive suffix product.
         for (int lo = 0; lo < p; lo += TCH) {
+            refresh();
             const int hi = lo + TCH < p ? lo + TCH : p;
             const bool mine = lo + ts < hi;
-            float av[8], kv[8], uv[8];
-            unpack_h8(ra, av);
-            unpack_h8(rk, kv);
-            unpack_h8(ru, uv);
-            if (!GATE) av[0] = h2f((uint16_t)ra.x);
+            // the record (copied into LDS by this same thread) stays packed in
+            // registers; halves are converted where stored
+            uint4 rk = make_uint4(0, 0, 0, 0), ru = rk, ra = rk;
+            if (mine) {
+                rk = raw[0][ts][l16];
+                ru = raw[1][ts][l16];
+                if (GATE) ra = raw[2][ts][l16];
+                else ra.x = ras;
+            }
+            auto h8 = [](const uint4 &w, int j) {
+                const uint32_t x = j < 2 ? w.x : j < 4 ? w.y : j < 6 ? w.z : w.w;
+                return h2f((uint16_t)(x >> (16 * (j & 1))));
+            };
             if (GATE) {
 #pragma unroll
-                for (int j = 0; j < 8; ++j) sh.bp[ts][KP(l16, j)] = mine ? av[j] : 1.0f;
+                for (int j = 0; j < 8; ++j) sh.bp[ts][KP(l16, j)] = mine ? h8(ra, j) : 1.0f;
             } else if (l16 == 0) {
-                sh.bp[ts][0] = mine ? av[0] : 1.0f;
+                sh.bp[ts][0] = mine ? h2f((uint16_t)ra.x) : 1.0f;
             }
             __syncthreads();
             if (tid < D) {
                 const int ch = GATE ? tid : 0;
-                float bv[TCH];
-#pragma unroll
-                for (int sl = 0; sl < TCH; ++sl) bv[sl] = sh.bp[sl][ch];
                 double c = 1.0;
 #pragma unroll
                 for (int sl = TCH - 1; sl >= 0; --sl) {
+                    const float bv = sh.bp[sl][ch];
                     if (GATE || tid == 0) sh.pre[sl][ch] = c;
-                    c *= (double)bv[sl];
+                    c *= (double)bv;
                 }
                 if (GATE || tid == 0) sh.tot[ch] = c;
             }
             __syncthreads();
+            if (mine) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const double P = sh.pre[ts][GATE ? KP(l16, j) : 0];
-                sh.key[ts][KP(l16, j)] = mine ? P * (double)kv[j] : 0.0;
-                sh.val[ts][8 * l16 + j] = mine ? uv[j] : 0.0f;
+                for (int j = 0; j < 8; ++j) {
+                    const double P = sh.pre[ts][GATE ? KP(l16, j) : 0];
+                    sh.key[ts][KP(l16, j)] = P * (double)h8(rk, j);
+                    sh.val[ts][8 * l16 + j] = h8(ru, j);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    sh.key[ts][KP(l16, j)] = 0.0;
+                    sh.val[ts][8 * l16 + j] = 0.0f;
+                }
             }
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
@@ -334,31 +368,26 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
 #pragma unroll
                 for (int b = 0; b < VPT; ++b) m[a][b] *= T;
             }
-            if (hi < p) load_pass(hi, hi + TCH < p ? hi + TCH : p);
             __syncthreads();
-            // records two at a time (a pass holds zeros past its last record),
-            // so one record's LDS reads overlap the other's FMAs
+            // sh.pre has been read by every thread: the next pass may land there
+            if (hi < p) load_pass(hi, hi + TCH < p ? hi + TCH : p);
+            // one record at a time, one key channel at a time, so only the
+            // record's 8 values and one key are live beside the block
             const int nrec = hi - lo;
 #pragma unroll 1
-            for (int j = 0; j < nrec; j += 2) {
-                double k0[8], k1[8], u0[VPT], u1[VPT];
-#pragma unroll
-                for (int a = 0; a < 8; ++a) k0[a] = sh.key[j][KP(kb, a)];
+            for (int j = 0; j < nrec; ++j) {
+                refresh();
+                double u0[VPT];
 #pragma unroll
                 for (int b = 0; b < VPT; ++b) u0[b] = (double)sh.val[j][VPT * vb + b];
 #pragma unroll
-                for (int a = 0; a < 8; ++a) k1[a] = sh.key[j + 1][KP(kb, a)];
+                for (int a = 0; a < 8; ++a) {
+                    const double k0 = sh.key[j][KP(kb, a)];
 #pragma unroll
-                for (int b = 0; b < VPT; ++b) u1[b] = (double)sh.val[j + 1][VPT * vb + b];
-#pragma unroll
-                for (int a = 0; a < 8; ++a)
-#pragma unroll
-                    for (int b = 0; b < VPT; ++b) m[a][b] = fma(k0[a], u0[b], m[a][b]);
-#pragma unroll
-                for (int a = 0; a < 8; ++a)
-#pragma unroll
-                    for (int b = 0; b < VPT; ++b) m[a][b] = fma(k1[a], u1[b], m[a][b]);
+                    for (int b = 0; b < VPT; ++b) m[a][b] = fma(k0, u0[b], m[a][b]);
+                }
             }
+            wait_vm_all();      // the next pass's records have landed in LDS
             __syncthreads();
         }
 
@@ -376,36 +405,36 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
 
     // ------------------------------------------------------------------ quantize
     for (int h = 0; h < r; ++h) {
-        double xa[8], p8[8];
+        refresh();
         // start vector: key-row l2 norms of the current residual
 #pragma unroll
         for (int a = 0; a < 8; ++a) {
             double s = 0.0;
 #pragma unroll
             for (int b = 0; b < VPT; ++b) s = fma(m[a][b], m[a][b], s);
-            p8[a] = s;
+            put_part(sh, a, s, kb, vb);
         }
-        double x = sqrt(reduce_over_values(sh, p8, kb, vb));
-        double nrm = sqrt(publish_vector(sh, x, xa, kb));
+        double x = sqrt(sum_parts(sh));
+        double nrm = sqrt(publish(sh, x, true));
         bool ok = nrm > 0.0;
-        if (ok) {
-            const double inv = 1.0 / nrm;
-#pragma unroll
-            for (int a = 0; a < 8; ++a) xa[a] *= inv;
-        }
+        // the published vector is read as sh.vec * xs: 1 / |x| after a
+        // normalisation, 1 between sweeps
+        double xs = ok ? 1.0 / nrm : 0.0;
         // Sweeps without per-sweep normalisation: each sweep is scaled by the
         // power of two sc ~ 1/|M|_F^2 (exact, so only the direction matters)
         // and the vector is normalised once after the last sweep.  A sweep
         // grows the norm by at most sc*sigma_1^2 < 2.
         const double sc = ok ? ldexp(1.0, -ilogb(nrm * nrm)) : 0.0;
         for (int it = 0; ok && it < A.power_iters; ++it) {
+            refresh();
             double y[VPT];
 #pragma unroll
-            for (int b = 0; b < VPT; ++b) {
-                double s = 0.0;
+            for (int b = 0; b < VPT; ++b) y[b] = 0.0;
 #pragma unroll
-                for (int a = 0; a < 8; ++a) s = fma(m[a][b], xa[a], s);
-                y[b] = s;
+            for (int a = 0; a < 8; ++a) {
+                const double xa = sh.vec[KP(kb, a)] * xs;
+#pragma unroll
+                for (int b = 0; b < VPT; ++b) y[b] = fma(m[a][b], xa, y[b]);
             }
             row_sum8(sh, y, kb, vb, sc);            // y_v = sc * sum_k M_kv x_k
 #pragma unroll
@@ -413,93 +442,87 @@ __global__ __launch_bounds__(TT, 2) void tile_kernel(TileArgs A) {
                 double s = 0.0;
 #pragma unroll
                 for (int b = 0; b < VPT; ++b) s = fma(m[a][b], y[b], s);
-                p8[a] = s;
+                put_part(sh, a, s, kb, vb);
             }
-            x = reduce_over_values(sh, p8, kb, vb);      // x_k = sum_v M_kv y_v
+            x = sum_parts(sh);                      // x_k = sum_v M_kv y_v
             if (it + 1 < A.power_iters) {
-                publish_only(sh, x, xa, kb);
+                publish(sh, x, false);
+                xs = 1.0;
             } else {
-                nrm = sqrt(publish_vector(sh, x, xa, kb));
+                nrm = sqrt(publish(sh, x, true));
                 ok = nrm > 0.0;
-                if (ok) {
-                    const double inv = 1.0 / nrm;
-#pragma unroll
-                    for (int a = 0; a < 8; ++a) xa[a] *= inv;
-                }
+                xs = ok ? 1.0 / nrm : 0.0;
             }
         }
-        uint16_t kh[8], uh[VPT];
+        // the pair, FP16 bits packed two per word (zero when the residual is zero)
+        // the pair, FP16 bits packed two per word, stored as soon as it is known
+        // (zero when the residual is zero)
+        refresh();
         if (ok) {
-            double kf[8], uf[VPT];
+            float kf[8];
+            uint32_t kw[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
-                kh[a] = d2h_via_f32(xa[a]);          // rounded through fp32
-                kf[a] = (double)h2f(kh[a]);
+                const uint16_t kh = d2h_via_f32(sh.vec[KP(kb, a)] * xs);   // rounded through fp32
+                kw[a >> 1] |= (uint32_t)kh << (16 * (a & 1));
+                kf[a] = h2f(kh);
             }
+            if (vb == 0)
+                *(uint4 *)(A.comp_k + ((size_t)tile * r + h) * D + 8 * kb) = make_uint4(kw[0], kw[1], kw[2], kw[3]);
             double us[VPT];
 #pragma unroll
             for (int b = 0; b < VPT; ++b) {
                 double s = 0.0;
 #pragma unroll
-                for (int a = 0; a < 8; ++a) s = fma(m[a][b], kf[a], s);
+                for (int a = 0; a < 8; ++a) s = fma(m[a][b], (double)kf[a], s);
                 us[b] = s;
             }
             row_sum8(sh, us, kb, vb, 1.0);
+            float uf[VPT];
+            uint32_t uw[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
             for (int b = 0; b < VPT; ++b) {
-                uh[b] = d2h_via_f32(us[b]);          // u~_v = fp16(sum_k M_kv k~_k)
-                uf[b] = (double)h2f(uh[b]);
+                const uint16_t uh = d2h_via_f32(us[b]);      // u~_v = fp16(sum_k M_kv k~_k)
+                uw[b >> 1] |= (uint32_t)uh << (16 * (b & 1));
+                uf[b] = h2f(uh);
             }
+            refresh();
+            if (kb == 0)
+                *(uint4 *)(A.comp_u + ((size_t)tile * r + h) * D + VPT * vb) = make_uint4(uw[0], uw[1], uw[2], uw[3]);
 #pragma unroll
             for (int a = 0; a < 8; ++a)
 #pragma unroll
-                for (int b = 0; b < VPT; ++b) m[a][b] = fma(-kf[a], uf[b], m[a][b]);
+                for (int b = 0; b < VPT; ++b) m[a][b] = fma(-(double)kf[a], (double)uf[b], m[a][b]);
         } else {
-#pragma unroll
-            for (int a = 0; a < 8; ++a) kh[a] = 0;
-#pragma unroll
-            for (int b = 0; b < VPT; ++b) uh[b] = 0;
-        }
-        if (vb == 0) {
-            uint4 w;
-            w.x = kh[0] | ((uint32_t)kh[1] << 16);
-            w.y = kh[2] | ((uint32_t)kh[3] << 16);
-            w.z = kh[4] | ((uint32_t)kh[5] << 16);
-            w.w = kh[6] | ((uint32_t)kh[7] << 16);
-            *(uint4 *)(A.comp_k + ((size_t)tile * r + h) * D + 8 * kb) = w;
-        }
-        if (kb == 0) {
-            uint4 w;
-            w.x = uh[0] | ((uint32_t)uh[1] << 16);
-            w.y = uh[2] | ((uint32_t)uh[3] << 16);
-            w.z = uh[4] | ((uint32_t)uh[5] << 16);
-            w.w = uh[6] | ((uint32_t)uh[7] << 16);
-            *(uint4 *)(A.comp_u + ((size_t)tile * r + h) * D + VPT * vb) = w;
+            if (vb == 0)
+                *(uint4 *)(A.comp_k + ((size_t)tile * r + h) * D + 8 * kb) = make_uint4(0u, 0u, 0u, 0u);
+            if (kb == 0)
+                *(uint4 *)(A.comp_u + ((size_t)tile * r + h) * D + VPT * vb) = make_uint4(0u, 0u, 0u, 0u);
         }
     }
 
+    refresh();
     // residual smoothing over key rows: c_k = sqrt(max(mean_v |R_kv|, 1e-12)) in fp32
-    double csd[8];
     {
-        double p8[8];
 #pragma unroll
         for (int a = 0; a < 8; ++a) {
             double s = 0.0;
 #pragma unroll
             for (int b = 0; b < VPT; ++b) s += fabs(m[a][b]);
-            p8[a] = s;
+            put_part(sh, a, s, kb, vb);
         }
-        const double s = reduce_over_values(sh, p8, kb, vb);
+        const double s = sum_parts(sh);
         float c = 1.0f;
         if (A.smooth_on) c = (float)sqrt(fmax(s * (1.0 / (double)D), (double)1e-12f));
         if (tid < D) A.smooth[tvec + KCH(tid)] = c;
-        publish_vector(sh, (double)c, csd, kb);
+        publish(sh, (double)c, false);
     }
+    refresh();
     // per-value-channel scale and codes, decided in fp32
     constexpr float QMAX = CodeFmt<CODE>::QMAX;
     float ic[8];
 #pragma unroll
-    for (int a = 0; a < 8; ++a) ic[a] = 1.0f / (float)csd[a];
+    for (int a = 0; a < 8; ++a) ic[a] = 1.0f / (float)sh.vec[KP(kb, a)];
 #pragma unroll
     for (int b = 0; b < VPT; ++b) {
         float rc[8];
