@@ -172,3 +172,22 @@ def test_packed_code_sizes_and_layout():
     g = 1 | (0x3F << 6) | (2 << 12) | (0x3E << 18)          # 24-bit group 0
     assert p6.shape == (96,) and list(p6[:3]) == [g & 0xFF, (g >> 8) & 0xFF, g >> 16]
     assert not p6[3:].any()
+
+
+def test_request_group_views():
+    """State.requests: a group of requests as views into the whole state, every
+    array starting at the group's first tile, the error word shared."""
+    d = B.make_dims(3, 5, 5, window=21, n_comp=4)
+    st = B.State.empty(d, device="cpu")
+    v = st.requests(1, 3)
+    assert (v.dims.batch, v.dims.heads_v, v.dims.window, v.dims.n_comp) == (2, 5, 21, 4)
+    assert d.batch == 3                                   # the whole state's dims are untouched
+    nb = dict(zip(B.FIELDS, B.leapquant_state_bytes(d)))
+    for f in B.FIELDS:
+        off = getattr(v, f).data_ptr() - getattr(st, f).data_ptr()
+        assert off == (0 if f == "err" else nb[f] // 3), f   # one request of three
+    assert (v.rec_len.data_ptr() - st.rec_len.data_ptr()) % 16 == 4      # 4-byte aligned only
+    assert (v.rec_a.data_ptr() - st.rec_a.data_ptr()) % 4 == 2           # 2-byte aligned only
+    for b0, b1 in ((2, 2), (-1, 1), (0, 4)):
+        with pytest.raises(ValueError):
+            st.requests(b0, b1)
