@@ -21,10 +21,13 @@
  *    commit mask need 4-byte alignment, the scalar gate's rec_a 2-byte
  *    alignment.  So one step of a step-major token buffer, or a state whose
  *    arrays all start at the same tile of a larger one (a group of requests),
- *    can be passed for any tile count.  The library allocates no memory, keeps no global state
- *    and never synchronises (except leapquant_check_error).  Work is enqueued on
+ *    can be passed for any tile count.
+ *  - The library allocates no memory, keeps no global state and never
+ *    synchronises (except leapquant_check_error).  Work is enqueued on
  *    `stream` (a hipStream_t; NULL = the default stream) and returns at once.
- *    Calls on different streams with disjoint buffers may run concurrently.
+ *    Calls on different streams with disjoint buffers may run concurrently
+ *    (request groups of one state share only its error word, which the
+ *    kernels update atomically).
  *  - The state of one tile is stored TRANSPOSED (value-major): row v holds the
  *    d_k key-channel entries of value channel v, S^T[v][k].
  *  - Status codes: LQ_OK (0) or a negative LQ_E* value.  Arguments are
