@@ -24,7 +24,8 @@ def test_f16_rounding_matches_numpy(O):
     r = (rng.standard_normal(2_000_000) * np.exp(rng.uniform(-25, 12, 2_000_000))).astype(np.float32)
     x = np.concatenate([x, r, np.float32([np.inf, -np.inf, 0.0, -0.0])])
     ours = O.f32_to_f16_bits(x)
-    ref = x.astype(np.float16).view(np.uint16)
+    with np.errstate(over="ignore"):             # values past the FP16 range round to infinity
+        ref = x.astype(np.float16).view(np.uint16)
     assert np.array_equal(ours, ref)
 
 
