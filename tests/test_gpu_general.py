@@ -31,6 +31,8 @@ CASES = {
                                 window=64, n_comp=8, code=synth.CODE_E4M3),
     "rwkv7_w21_int4": GEN.with_(name="rwkv7_w21_int4", batch=2, heads_v=4, heads_k=4, steps=84,
                                 window=21, n_comp=8, code=synth.CODE_INT4),
+    "rwkv7_w32_int6": GEN.with_(name="rwkv7_w32_int6", batch=2, heads_v=4, heads_k=4, steps=64,
+                                window=32, n_comp=4, code=synth.CODE_INT6),
     # scalar gate, arbitrary read vectors, 100 records per window (two record passes)
     "general_gdn_w100": GEN.with_(name="general_gdn_w100", batch=2, heads_v=4, heads_k=4, steps=200,
                                   window=100, n_comp=8, gate=synth.GATE_SCALAR),

@@ -51,6 +51,10 @@ SMALL = {
     "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1),
     "gla_small": W_["kda_kimi"].with_(name="gla_small", batch=2, heads_v=4, heads_k=4, steps=128,
                                       prefill=256, rule=1),
+    # the same rows with the other code formats
+    "mamba2_e4m3": W_["gdn_tiny"].with_(name="mamba2_e4m3", rule=1, code=synth.CODE_E4M3),
+    "gla_int6": W_["kda_kimi"].with_(name="gla_int6", batch=2, heads_v=4, heads_k=4, steps=64, window=32,
+                                     n_comp=4, prefill=128, rule=1, code=synth.CODE_INT6),
 }
 
 
