@@ -53,6 +53,7 @@ SMALL = {
                                       prefill=256, rule=1),
     # the same rows with the other code formats
     "mamba2_e4m3": W_["gdn_tiny"].with_(name="mamba2_e4m3", rule=1, code=synth.CODE_E4M3),
+    "mamba2_int4": W_["gdn_tiny"].with_(name="mamba2_int4", rule=1, code=synth.CODE_INT4, n_comp=8),
     "gla_int6": W_["kda_kimi"].with_(name="gla_int6", batch=2, heads_v=4, heads_k=4, steps=64, window=32,
                                      n_comp=4, prefill=128, rule=1, code=synth.CODE_INT6),
 }
