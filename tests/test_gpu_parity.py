@@ -33,6 +33,9 @@ SMALL = {
                                            steps=64, prefill=128),
     "kda_w16_r4": W_["kda_kimi"].with_(name="kda_w16_r4", batch=2, heads_v=4, heads_k=4, steps=64,
                                        window=16, n_comp=4, prefill=128),
+    # per-channel gate with grouped key heads (two value heads per key head) and E4M3 codes
+    "kda_gqa_e4m3": W_["kda_kimi"].with_(name="kda_gqa_e4m3", batch=2, heads_v=4, heads_k=2, steps=64,
+                                         window=32, n_comp=8, prefill=128, code=synth.CODE_E4M3),
     "kda_int4_small": W_["kda_kimi"].with_(name="kda_int4_small", batch=2, heads_v=4, heads_k=4,
                                            steps=128, prefill=256, code=synth.CODE_INT4),
     "gdn_int6_small": W_["gdn_tiny"].with_(name="gdn_int6_small", code=synth.CODE_INT6),
