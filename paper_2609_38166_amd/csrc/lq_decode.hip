@@ -5,13 +5,27 @@
 //           + U~ (K~^T (Gamma_{1:i} x))                     Compensator Tokens
 //           + sum_{j<i} u_j (k~_j^T (Gamma_{j+1:i} x))      buffered records
 // for x = k_t and x = q_t in one pass over the codes (App. B.2 Eq. (readout),
-// App. B.3 Eq. (smooth-readout)) -- the code product on the matrix cores, see
-// below -- then forms u_t = fp16(v_t - A^T k_t), the
-// output o_t = A^T q_t + u_t (k~_t . q_t) (post-update state, Sec. 3.1) and
-// appends the record (alpha_t, k~_t, u_t) (Sec. 3.2 Eq. (record)).
-// Under the general rule (read vector b_t given, App. A) the same pass reads
-// S_{i-1}^T x, i.e. the decays Gamma_{.:i-1} without this token's, for x = b_t
-// and x = d_t . q_t (d_t the FP16 decay), and u_t = fp16(v_t - S_{i-1}^T b_t).
+// App. B.3 Eq. (smooth-readout)), then forms the correction
+// u_t = fp16(v_t - A^T k_t), the output o_t = A^T q_t + u_t (k~_t . q_t)
+// (post-update state, Sec. 3.1) and appends the record (alpha_t, k~_t, u_t)
+// (Sec. 3.2 Eq. (record)).  Under the general rule (read vector b_t given,
+// App. A) the same pass reads S_{i-1}^T x, i.e. the decays Gamma_{.:i-1}
+// without this token's, for x = b_t and x = d_t . q_t (d_t the FP16 decay),
+// and u_t = fp16(v_t - S_{i-1}^T b_t).
+//
+// Precision.  The correction is rounded to FP16 and stored; every later step
+// and the window-end refit read the rounded value, so a rounding decision
+// taken differently here changes the state.  The k side (the readout that
+// feeds u_t) is therefore carried at fp64 accuracy, which makes u_t the
+// correctly rounded FP16 value of the exact expression except in cases of
+// probability ~1e-10: decay products, record and compensator readouts in
+// fp64, and the code product exact in integer arithmetic.  The read vector
+// w = c . Gamma x is written as a fixed-point number, an exponent per 64
+// channels and five base-128 digits (34 bits, each digit an int8), and
+// Z^T w is a sum of int8 x int8 dot products (v_dot4_i32_i8) per digit,
+// combined in fp64 exactly.  The q side, which only feeds the output, uses
+// three digits and fp32.  E4M3 codes are not integers; their product is
+// taken in fp64 (k side) and fp32 (q side) on the vector ALU.
 //
 // Every global load of the tile is issued before the first barrier: rec_len (a
 // scalar load, which the record loads wait for), the token inputs, the
@@ -19,11 +33,10 @@
 // and instruction, so they hold no registers), the compensators, then one pass
 // of records, loaded non-temporally (16 slots of 16 lanes, each slot a
 // contiguous block of records, 16 bytes of key, correction and decay per
-// lane).  The decays
-// Gamma_{j+1:i} are products of the FP16 record decays: each slot forms the
-// product of its block, one scan over the 16 slots gives every block the decay
-// of all newer records, and the slot walks its block from the newest record
-// back.  No d_k x d_v intermediate exists.
+// lane).  The decays Gamma_{j+1:i} are products of the FP16 record decays:
+// each slot forms the product of its block, one scan over the 16 slots gives
+// every block the decay of all newer records, and the slot walks its block
+// from the newest record back.  No d_k x d_v intermediate exists.
 #include "lq_device.hpp"
 #include "lq_internal.hpp"
 
@@ -33,21 +46,24 @@ namespace {
 
 constexpr int SLOTS = 16;            // 16-lane groups per workgroup
 // Records per slot and pass: the diagonal gate carries a 16-byte decay per lane
-// and record, so it holds three per slot (48 per pass) to stay within 128
-// VGPRs (4 resident workgroups per CU); the scalar gate holds four (64 per pass).
+// and record, so it holds three per slot (48 per pass); the scalar gate holds
+// four (64 per pass).
 template <int GATE> struct Pass {
     static constexpr int PER_SLOT = GATE ? 3 : 4;
     static constexpr int N = SLOTS * PER_SLOT;
 };
 
-// Per-channel vectors that the slots read or write 8 channels at a time are
-// kept in LDS in a swizzled order: channel 8*l16 + j sits at position
-// 16*j + l16, so for each j the 16 lanes of a slot touch 16 consecutive words.
-// Per-slot rows are padded by 16 words, which puts the 4 slots of a wave in
-// different bank groups.  A thread t < D that works on a whole vector (the
-// scan, the base vectors, the final combine) owns position t, i.e. channel
-// CH(t); POS is the inverse map.
-constexpr int RP = D + 16;                       // padded per-slot row
+// Base-128 digits of the read vectors of the code product.
+constexpr int KDIG = 5;              // k side: 6 + 4 x 7 = 34 bits
+constexpr int QDIG = 3;              // q side: 20 bits
+constexpr int NDIG = KDIG + QDIG;
+
+// Per-channel vectors that the slots read 8 channels at a time are kept in LDS
+// in a swizzled order: channel 8*l16 + j sits at position 16*j + l16, so for
+// each j the 16 lanes of a slot touch 16 consecutive words.  A thread t < D
+// that works on a whole vector (the scan, the base vectors, the final combine)
+// owns position t, i.e. channel CH(t); POS is the inverse map.  Threads
+// 0..63 own the channels c with (c & 7) < 4, threads 64..127 the others.
 __device__ __forceinline__ constexpr int SW(int l16, int j) { return 16 * j + l16; }
 __device__ __forceinline__ constexpr int CH(int t) { return 8 * (t & 15) + (t >> 4); }
 __device__ __forceinline__ constexpr int POS(int c) { return 16 * (c & 7) + (c >> 3); }
@@ -86,15 +102,32 @@ struct RecRegs {
     uint32_t as[PER_SLOT];           // FP16 decay (scalar gate), converted where used
 };
 
-
 // Non-temporal 16-byte load, for the records: a step streams every tile's
 // buffered records once, and as plain loads they would evict the codes from
 // the last-level (Infinity) cache, where a batch's codes can stay resident
-// from one step to the next (134 MB of int8 codes at 8192 tiles).
+// from one step to the next.
 __device__ __forceinline__ uint4 ld_stream16(const uint16_t *p) {
     typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
     return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ double h2d(uint32_t w, int hi) {
+    return (double)h2f((uint16_t)(w >> (16 * hi)));
+}
+
+// Cross-row swaps of a double (two 32-bit halves).
+__device__ __forceinline__ void swap32_d(double a, double b, double &ra, double &rb) {
+    const auto lo = __builtin_amdgcn_permlane32_swap(__double2loint(a), __double2loint(b), false, false);
+    const auto hi = __builtin_amdgcn_permlane32_swap(__double2hiint(a), __double2hiint(b), false, false);
+    ra = __hiloint2double(hi[0], lo[0]);
+    rb = __hiloint2double(hi[1], lo[1]);
+}
+__device__ __forceinline__ void swap16_d(double a, double b, double &ra, double &rb) {
+    const auto lo = __builtin_amdgcn_permlane16_swap(__double2loint(a), __double2loint(b), false, false);
+    const auto hi = __builtin_amdgcn_permlane16_swap(__double2hiint(a), __double2hiint(b), false, false);
+    ra = __hiloint2double(hi[0], lo[0]);
+    rb = __hiloint2double(hi[1], lo[1]);
 }
 
 // Sum of x over the 4 slots (16-lane rows) of a wave, for 8 values per lane,
@@ -115,59 +148,64 @@ __device__ __forceinline__ void rows4_reduce_scatter(const float *x, float &s0, 
     s0 = __uint_as_float(r0[0]) + __uint_as_float(r0[1]);
     s1 = __uint_as_float(r1[0]) + __uint_as_float(r1[1]);
 }
-
-// The read vectors of the code product, w = c . Gamma_{1:i} x, as three bf16
-// parts with w = hi + mid + lo exactly: hi and mid keep the leading 8
-// significant bits of w and of w - hi (truncation, so both differences are
-// exact in fp32), and the remainder has at most 8 significant bits left.
-// s_wb[part][0 = k_t, 1 = q_t][channel], bf16 bits.
-__device__ __forceinline__ void split_bf16x3(float w, uint16_t (*s_wb)[2][D], int vec, int c) {
-    const uint32_t hi = __float_as_uint(w) & 0xFFFF0000u;
-    const float r1 = w - __uint_as_float(hi);
-    const uint32_t mid = __float_as_uint(r1) & 0xFFFF0000u;
-    const float r2 = r1 - __uint_as_float(mid);
-    s_wb[0][vec][c] = (uint16_t)(hi >> 16);
-    s_wb[1][vec][c] = (uint16_t)(mid >> 16);
-    s_wb[2][vec][c] = f2bf(r2);
+__device__ __forceinline__ void rows4_reduce_scatter(const double *x, double &s0, double &s1) {
+    double h[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        double a, b;
+        swap32_d(x[i], x[4 + i], a, b);
+        h[i] = a + b;
+    }
+    double a, b;
+    swap16_d(h[0], h[2], a, b);
+    s0 = a + b;
+    swap16_d(h[1], h[3], a, b);
+    s1 = a + b;
 }
 
-// y = Gamma_{1:i} x (swizzled) and the split of w = c . y (channel order) for
-// x = k_t, q_t; thread t < D: channel CH(t).
-__device__ __forceinline__ void write_base_vectors(float G, float kx, float qx, float cs, float (*s_y)[D],
-                                                   uint16_t (*s_wb)[2][D], int t) {
-    const float yk = G * kx, yq = G * qx;
-    s_y[0][t] = yk;
-    s_y[1][t] = yq;
-    split_bf16x3(cs * yk, s_wb, 0, CH(t));
-    split_bf16x3(cs * yq, s_wb, 1, CH(t));
+// Largest value of x over the 64 lanes of the wave (uniform result).
+__device__ __forceinline__ int wave_max_i32(int x) {
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_XOR1, 0xF, 0xF, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_XOR2, 0xF, 0xF, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_ROR4, 0xF, 0xF, false));
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_ROR8, 0xF, 0xF, false));
+    const int a = max(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16));
+    const int b = max(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48));
+    return max(a, b);
 }
 
 // Code rows in LDS are stored in 16-byte chunks, each row rotated by zrot(v)
-// chunks, so that the 16 rows a matrix-core operand reads at one chunk
-// position fall in distinct banks.  The rotation is applied when the copy is
-// issued (lane L's destination is fixed; its source chunk is chosen).  The
-// 6-bit rows (96 bytes, 16 codes = 12 bytes) are not rotated.
+// chunks, so that the lanes of a code-product read (consecutive rows, two
+// halves of each) fall in distinct banks.  The rotation is applied when the
+// copy is issued (lane L's destination is fixed; its source chunk is
+// chosen).  The 6-bit rows (96 bytes) are not rotated.
+template <int CODE> struct Rows {
+    static constexpr int BYTES = D * CodeFmt<CODE>::BITS / 8;
+    static constexpr int SEGS = BYTES / 16;                 // 16-byte chunks per row
+};
 template <int CODE> __device__ __forceinline__ int zrot(int v) {
-    return CODE == 3 ? 0 : (CODE == 2 ? (v >> 2) & 3 : (v >> 1) & 7);
+    return CODE == 3 ? 0 : (v & (Rows<CODE>::SEGS - 1));
 }
-
-// Codes 16 s .. 16 s + 15 of row v from the rotated LDS copy.
+// Chunk c (global numbering) of row v from the rotated LDS copy.
 template <int CODE>
-__device__ __forceinline__ uint4 lds_codes16(const uint4 *z, int v, int s) {
-    constexpr int SEGS = D * CodeFmt<CODE>::BITS / 8 / 16;     // chunks per row
-    if (CODE <= 1) return z[v * SEGS + ((s + zrot<CODE>(v)) & (SEGS - 1))];
-    if (CODE == 2) {
-        const uint2 *h = (const uint2 *)&z[v * SEGS + (((s >> 1) + zrot<CODE>(v)) & (SEGS - 1))];
-        const uint2 w = h[s & 1];
-        return make_uint4(w.x, w.y, 0u, 0u);
-    }
-    const uint32_t *w = (const uint32_t *)((const uint8_t *)z + v * (SEGS * 16) + 12 * s);
-    return make_uint4(w[0], w[1], w[2], 0u);
+__device__ __forceinline__ uint4 lds_chunk(const uint4 *z, int v, int c) {
+    constexpr int SEGS = Rows<CODE>::SEGS;
+    if (CODE == 3) return z[v * SEGS + c];
+    return z[v * SEGS + ((c + zrot<CODE>(v)) & (SEGS - 1))];
 }
 
-// bf16 bits of two small exact floats, packed low | high << 16.
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+// Four signed 4-bit codes (a 16-bit field of nibbles) as four int8 bytes:
+// bytes b0 b1 of h16 = (n1 n0), (n3 n2) become n0, n1, n2, n3, each sign
+// extended through (n ^ 8) + 0x78 ^ 0x80 per byte (no carry between bytes).
+__device__ __forceinline__ uint32_t int4x4_to_bytes(uint32_t w, int half) {
+    const uint32_t p = __builtin_amdgcn_perm(w, w, half ? 0x03030202u : 0x01010000u);
+    const uint32_t t = (p & 0x000F000Fu) | ((p >> 4) & 0x0F000F00u);
+    return ((t ^ 0x08080808u) + 0x78787878u) ^ 0x80808080u;
+}
+// Four signed 6-bit codes (a 24-bit field) as four int8 bytes.
+__device__ __forceinline__ uint32_t int6x4_to_bytes(uint32_t g) {
+    const uint32_t t = (g & 0x3Fu) | ((g << 2) & 0x3F00u) | ((g << 4) & 0x3F0000u) | ((g << 6) & 0x3F000000u);
+    return ((t ^ 0x20202020u) + 0x60606060u) ^ 0x80808080u;
 }
 
 template <int GATE>
@@ -186,26 +224,185 @@ __device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, 
     }
 }
 
+// LDS of one tile.  The decay array s_bp is reused at the end: wave w writes
+// its partial readouts into rows 4w .. 4w+3, which only its own slots read.
+template <int CODE>
+struct DecodeShared {
+    static constexpr int ZCH = D * Rows<CODE>::BYTES / 16;   // 16-byte chunks of a tile's codes
+    float x[2][D];                 // x = k_t, q_t (swizzled)
+    double yk[D];                  // Gamma_{1:i} . x_k (swizzled), for the compensators
+    float yq[D];                   // Gamma_{1:i} . x_q (swizzled)
+    double zk[D];                  // code readout delta . Z^T w, k side (by position)
+    float zq[D];                   // q side
+    float kq[2];                   // k~_t . q_t (per wave)
+    int ex[2][2];                  // digit exponents [k, q][scan wave]
+    double pre0[SLOTS];            // scalar gate: decay of everything newer than a slot's block
+    // read vectors of the code product: NDIG digit rows of D int8 (integer
+    // codes), or w_k (fp64) and w_q (fp32) (E4M3), channel order
+    __align__(16) uint8_t rv[D * 8 + D * 4];
+    __align__(16) double bp[SLOTS][D];   // decay products (swizzled); later the wave partials
+    __align__(16) uint4 codes[ZCH];      // the tile's codes, rows rotated by zrot
+    __align__(16) float dlt[D];          // the tile's per-row scales
+};
+
+// The read vectors of the code product for channel ch (thread t < D):
+// w_k = c . y_k and w_q = c . y_q, with y = Gamma_{1:i} x.
+template <int CODE, bool KS>
+__device__ __forceinline__ void base_vectors(DecodeShared<CODE> &sh, double G, float kx, float qx, float cs,
+                                             int t) {
+    const int ch = CH(t);
+    const double yk = G * (double)kx, yq = G * (double)qx;
+    sh.yk[t] = yk;
+    sh.yq[t] = (float)yq;
+    const double wk = (double)cs * yk, wq = (double)cs * yq;
+    if (CODE == 1) {
+        double *wkv = (double *)sh.rv;
+        float *wqv = (float *)(sh.rv + D * 8);
+        if (KS) wkv[ch] = wk;
+        wqv[ch] = (float)wq;
+        return;
+    }
+    // w = 2^(E - 6) * sum_d digit_d 128^-d with |w| < 2^E over the wave's 64
+    // channels, every digit in [-64, 64]: x - rint(x) is exact and in
+    // [-1/2, 1/2], and scaling by 128 is exact.
+    int8_t *dig = (int8_t *)sh.rv;
+    if (KS) {
+        const int e = wave_max_i32(__builtin_amdgcn_frexp_exp(wk));
+        double x = __builtin_ldexp(wk, 6 - e);
+#pragma unroll
+        for (int d = 0; d < KDIG; ++d) {
+            const double r = __builtin_rint(x);
+            dig[d * D + ch] = (int8_t)(int)r;
+            x = (x - r) * 128.0;
+        }
+        if ((t & 63) == 0) sh.ex[0][t >> 6] = e;
+    }
+    {
+        const int e = wave_max_i32(__builtin_amdgcn_frexp_exp(wq));
+        double x = __builtin_ldexp(wq, 6 - e);
+#pragma unroll
+        for (int d = 0; d < QDIG; ++d) {
+            const double r = __builtin_rint(x);
+            dig[(KDIG + d) * D + ch] = (int8_t)(int)r;
+            x = (x - r) * 128.0;
+        }
+        if ((t & 63) == 0) sh.ex[1][t >> 6] = e;
+    }
+}
+
+// Code product of one half row: thread (v, h) sums over channels 64h .. 64h+63
+// of row v.  Integer codes: per digit and per exponent group (g = (c >> 2) & 1,
+// the scan wave that set the exponent) an exact int32 sum of int8 products.
+template <int CODE, bool KS>
+__device__ __forceinline__ void code_product(const DecodeShared<CODE> &sh, int v, int h, double &zk, float &zq) {
+    if (CODE == 1) {
+        const double *wkv = (const double *)sh.rv;
+        const float *wqv = (const float *)(sh.rv + D * 8);
+        double sk = 0.0;
+        float sq = 0.0f;
+#pragma unroll 1
+        for (int m = 0; m < 4; ++m) {
+            const int c = 4 * h + m;
+            const uint4 z = lds_chunk<CODE>(sh.codes, v, c);
+            const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int c0 = 16 * c + 4 * p;         // channels c0 .. c0 + 3
+                const float4 wq = *(const float4 *)&wqv[c0];
+                const float f0 = e4m3_to_f<0>(zw[p]), f1 = e4m3_to_f<1>(zw[p]);
+                const float f2 = e4m3_to_f<2>(zw[p]), f3 = e4m3_to_f<3>(zw[p]);
+                sq = fmaf(f0, wq.x, sq);
+                sq = fmaf(f1, wq.y, sq);
+                sq = fmaf(f2, wq.z, sq);
+                sq = fmaf(f3, wq.w, sq);
+                if (KS) {
+                    const double2 wa = *(const double2 *)&wkv[c0], wb = *(const double2 *)&wkv[c0 + 2];
+                    sk = fma((double)f0, wa.x, sk);
+                    sk = fma((double)f1, wa.y, sk);
+                    sk = fma((double)f2, wb.x, sk);
+                    sk = fma((double)f3, wb.y, sk);
+                }
+            }
+        }
+        zk = sk;
+        zq = sq;
+        return;
+    }
+    constexpr int D0 = KS ? 0 : KDIG;            // first digit row used
+    const uint32_t *dig = (const uint32_t *)sh.rv;   // [NDIG][D / 4] words
+    int acc[NDIG][2];
+#pragma unroll
+    for (int d = 0; d < NDIG; ++d) acc[d][0] = acc[d][1] = 0;
+    // the 4-channel words of this half row as int8 bytes: word i holds
+    // channels 64h + 4i .. 64h + 4i + 3, exponent group i & 1
+    auto dot_word = [&](uint32_t zb, int i) {
+        const int g = i & 1;
+#pragma unroll
+        for (int d = D0; d < NDIG; ++d)
+            acc[d][g] = __builtin_amdgcn_sdot4((int)zb, (int)dig[d * (D / 4) + 16 * h + i], acc[d][g], false);
+    };
+    if (CODE == 0) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const uint4 z = lds_chunk<CODE>(sh.codes, v, 4 * h + m);
+            dot_word(z.x, 4 * m + 0);
+            dot_word(z.y, 4 * m + 1);
+            dot_word(z.z, 4 * m + 2);
+            dot_word(z.w, 4 * m + 3);
+        }
+    } else if (CODE == 2) {
+        // 32 codes per chunk, two chunks per half row; each word holds 8 channels
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const uint4 z = lds_chunk<CODE>(sh.codes, v, 2 * h + m);
+            const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                dot_word(int4x4_to_bytes(zw[p], 0), 8 * m + 2 * p);
+                dot_word(int4x4_to_bytes(zw[p], 1), 8 * m + 2 * p + 1);
+            }
+        }
+    } else {
+        // 48 bytes per half row, four units of 12 bytes = 4 groups of 3 bytes
+        const uint32_t *zr = (const uint32_t *)sh.codes + v * (Rows<CODE>::BYTES / 4) + 12 * h;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t w0 = zr[3 * u], w1 = zr[3 * u + 1], w2 = zr[3 * u + 2];
+            dot_word(int6x4_to_bytes(w0 & 0xFFFFFFu), 4 * u);
+            dot_word(int6x4_to_bytes(__builtin_amdgcn_alignbit(w1, w0, 24) & 0xFFFFFFu), 4 * u + 1);
+            dot_word(int6x4_to_bytes(__builtin_amdgcn_alignbit(w2, w1, 16) & 0xFFFFFFu), 4 * u + 2);
+            dot_word(int6x4_to_bytes(w2 >> 8), 4 * u + 3);
+        }
+    }
+    // sum_d acc_d 128^-d is exact in fp64 (|acc_d| < 2^19, 34 bits below)
+    double sk = 0.0;
+    if (KS) {
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+            double s = (double)acc[KDIG - 1][g];
+#pragma unroll
+            for (int d = KDIG - 2; d >= 0; --d) s = fma(s, 0x1p-7, (double)acc[d][g]);
+            sk += __builtin_ldexp(s, sh.ex[0][g] - 6);
+        }
+    }
+    float sq = 0.0f;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+        float s = (float)acc[NDIG - 1][g];
+#pragma unroll
+        for (int d = NDIG - 2; d >= KDIG; --d) s = fmaf(s, 0x1p-7f, (float)acc[d][g]);
+        sq += __builtin_ldexpf(s, sh.ex[1][g] - 6);
+    }
+    zk = sk;
+    zq = sq;
+}
+
 template <int GATE, int CODE, int RULE>
 __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
-    constexpr int GP = GATE ? RP : 1;
-    constexpr int ROWB = D * CodeFmt<CODE>::BITS / 8;   // code bytes per value row
-    constexpr int ZCH = D * ROWB / 16;                   // 16-byte chunks of a tile's codes
+    constexpr bool KS = RULE != LQ_RULE_ADD;     // the k side is read (not for b_t = 0)
+    constexpr int ZCH = DecodeShared<CODE>::ZCH;
     static_assert(ZCH % NT == 0, "whole chunks per thread");
-    __shared__ float s_x[2][D];          // x = k_t, q_t (swizzled)
-    __shared__ __align__(16) uint16_t s_wb[3][2][D];   // c . Gamma_{1:i} . x as bf16 parts
-    __shared__ float s_y[2][D];          // Gamma_{1:i} . x (swizzled)
-    __shared__ float s_z[2][D];          // quantized-residual readout (swizzled)
-    __shared__ float s_kq[2];            // k~_t . q_t (per wave pair)
-    // decay product of each slot's block, replaced in place by the decay of
-    // everything newer than the block (swizzled; the diagonal gate's thread t
-    // alone reads and writes position t).  The scalar gate's single product is
-    // read by every scan thread, so its prefix goes to s_pre0 instead.
-    __shared__ float s_bp[SLOTS][GP];
-    __shared__ float s_pre0[SLOTS];
-    __shared__ __align__(16) uint4 s_codes[ZCH];   // the tile's codes, row-major as in HBM
-    __shared__ __align__(16) float s_dlt[D];       // the tile's per-row scales
-    __shared__ __align__(16) float s_red[NT / 64][2][2 * 64];   // per-wave partial readouts, k then q
+    __shared__ DecodeShared<CODE> sh;
 
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -213,7 +410,6 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     // b H_k + h_v / group = tile / group, taken as a multiply by ceil(2^32 /
     // group) and a shift (exact while tiles * group < 2^32, which the launch
     // checks)
-
     const size_t tvec = (size_t)tile * D;
 
     const int l16 = tid & 15;            // 8-channel key segment / 8-value segment
@@ -252,16 +448,16 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     {
         // LDS chunk P = NT m + 64 w + L (wave w's lanes fill 1 KiB) holds chunk
         // (P - zrot(v)) mod SEGS of row v = P / SEGS
-        constexpr int SEGS = ROWB / 16;
-        const uint4 *zt = (const uint4 *)(a.codes + (size_t)tile * D * ROWB);
+        constexpr int SEGS = Rows<CODE>::SEGS;
+        const uint4 *zt = (const uint4 *)(a.codes + (size_t)tile * D * Rows<CODE>::BYTES);
         const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
         for (int m = 0; m < ZCH / NT; ++m) {
             const int P = NT * m + tid, v = P / SEGS, c = P - v * SEGS;
-            dma16(zt + v * SEGS + ((c - zrot<CODE>(v) + SEGS) % SEGS), lds_addr(&s_codes[NT * m + 64 * w]));
+            dma16(zt + v * SEGS + ((c - zrot<CODE>(v) + SEGS) % SEGS), lds_addr(&sh.codes[NT * m + 64 * w]));
         }
     }
-    if (tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(s_dlt));   // per-row scales, wave 0
+    if (tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(sh.dlt));   // per-row scales, wave 0
     uint4 ck = make_uint4(0, 0, 0, 0), cu = make_uint4(0, 0, 0, 0);
     if (ts < a.n_comp) {
         const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
@@ -287,145 +483,156 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     // ---- token inputs, this token's record -------------------------------------
     // carry: decay of every record newer than the current pass, channel ch
     // (the scalar gate keeps the same product in every thread below D)
-    float carry = 1.0f;
+    double carry = 1.0;
     if (tid < D) {
         const uint16_t ah = f2h(al);
         // read vectors: k_t and q_t under the decay of this token (carry), or
         // b_t and d_t . q_t read against S_{i-1} (carry starts at 1)
         const bool gen = RULE == LQ_RULE_GENERAL;
         const float xk = gen ? bx : kx, xq = gen ? h2f(ah) * qx : qx;
-        s_x[0][tid] = xk;
-        s_x[1][tid] = xq;
-        if (!gen) carry = h2f(ah);
+        sh.x[0][tid] = xk;
+        sh.x[1][tid] = xq;
+        if (!gen) carry = (double)h2f(ah);
         const size_t slot = rbase + n;
         if (GATE) a.rec_a[slot * D + ch] = ah;
         else if (tid == 0) a.rec_a[slot] = ah;
-        const uint16_t tkh = f2h(bt * kx);                   // k~_t = fp16(beta_t k_t)
+        const uint16_t tkh = f2h_mul(bt, kx);                // k~_t = fp16(fp32(beta_t k_t))
         a.rec_k[slot * D + ch] = tkh;
         const float kq = wave_sum(h2f(tkh) * qx);
-        if ((tid & 63) == 0) s_kq[tid >> 6] = kq;
+        if ((tid & 63) == 0) sh.kq[tid >> 6] = kq;
         kx = xk;                                             // the base vectors read these
         qx = xq;
     }
 
-    float acc_k[8], acc_q[8];
+    double acc_k[8];
+    float acc_q[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc_k[j] = acc_q[j] = 0.0f;
+    for (int j = 0; j < 8; ++j) {
+        acc_k[j] = 0.0;
+        acc_q[j] = 0.0f;
+    }
 
     // ---- buffered records, newest first, up to PASS per pass ----------------------
     if (n > 0) {
-        bool first = true;
-        float xk[8], xq[8];
         while (true) {
             // decay product of this slot's block, per channel of its segment
-            float bp[8];
+            // (up to three FP16 factors: exact in fp64)
+            if (GATE) {
+                double bp[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) bp[j] = 1.0f;
+                for (int j = 0; j < 8; ++j) bp[j] = 1.0;
 #pragma unroll
-            for (int q = 0; q < PER_SLOT; ++q) {
-                if (hi - 1 - (PER_SLOT * ts + q) >= lo) {
-                    if (GATE) {
-                        float av[8];
-                        unpack_h8(R.a[q], av);
+                for (int q = 0; q < PER_SLOT; ++q) {
+                    if (hi - 1 - (PER_SLOT * ts + q) >= lo) {
+                        const uint32_t w4[4] = {R.a[q].x, R.a[q].y, R.a[q].z, R.a[q].w};
 #pragma unroll
-                        for (int j = 0; j < 8; ++j) bp[j] *= av[j];
-                    } else {
-                        bp[0] *= h2f((uint16_t)R.as[q]);
+                        for (int j = 0; j < 8; ++j) bp[j] *= h2d(w4[j >> 1], j & 1);
                     }
                 }
-            }
-            if (GATE) {
 #pragma unroll
-                for (int j = 0; j < 8; ++j) s_bp[ts][SW(l16, j)] = bp[j];
-            } else if (l16 == 0) {
-                s_bp[ts][0] = bp[0];
+                for (int j = 0; j < 8; ++j) sh.bp[ts][SW(l16, j)] = bp[j];
+            } else {
+                double bp = 1.0;
+#pragma unroll
+                for (int q = 0; q < PER_SLOT; ++q)
+                    if (hi - 1 - (PER_SLOT * ts + q) >= lo) bp *= (double)h2f((uint16_t)R.as[q]);
+                if (l16 == 0) sh.bp[ts][0] = bp;
             }
             __syncthreads();
-            if (first) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    xk[j] = s_x[0][SW(l16, j)];
-                    xq[j] = s_x[1][SW(l16, j)];
-                }
-                first = false;
-            }
             // exclusive scan over the slots; slot 0 holds the newest block
             if (tid < D) {
-                float c = carry;
-                // slot products read ahead of the chain, then overwritten
-                float bv[SLOTS];
+                double c = carry;
+                // slot products read ahead of the chain (eight at a time), then
+                // overwritten
 #pragma unroll
-                for (int s = 0; s < SLOTS; ++s) bv[s] = s_bp[s][GATE ? tid : 0];
+                for (int s0 = 0; s0 < SLOTS; s0 += 8) {
+                    double bv[8];
 #pragma unroll
-                for (int s = 0; s < SLOTS; ++s) {
-                    if (GATE) s_bp[s][tid] = c;
-                    else if (tid == 0) s_pre0[s] = c;
-                    c *= bv[s];
+                    for (int s = 0; s < 8; ++s) bv[s] = sh.bp[s0 + s][GATE ? tid : 0];
+#pragma unroll
+                    for (int s = 0; s < 8; ++s) {
+                        if (GATE) sh.bp[s0 + s][tid] = c;
+                        else if (tid == 0) sh.pre0[s0 + s] = c;
+                        c *= bv[s];
+                    }
                 }
                 carry = c;
-                if (lo == 0) write_base_vectors(carry, kx, qx, cs, s_y, s_wb, tid);   // carry = Gamma_{1:i}
+                if (lo == 0) base_vectors<CODE, KS>(sh, carry, kx, qx, cs, tid);   // carry = Gamma_{1:i}
             }
             if (lo == 0) wait_vm_all();  // this wave's code copies have landed
             __syncthreads();
             if (GATE) {
-                float P[8];
+                // Y = Gamma_{j+1:i} . x for the slot's newest record, then older
+                double Yk[8];
+                float Yq[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) P[j] = s_bp[ts][SW(l16, j)];
+                for (int j = 0; j < 8; ++j) {
+                    const double P = sh.bp[ts][SW(l16, j)];
+                    Yk[j] = P * (double)sh.x[0][SW(l16, j)];
+                    Yq[j] = (float)P * sh.x[1][SW(l16, j)];
+                }
 #pragma unroll
                 for (int q = 0; q < PER_SLOT; ++q) {
                     if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
-                    // products with an FP16 operand are written as fma(h, x, 0), which
-                    // takes the half directly (same value as the product)
-                    float kv[8], uv[8];
+                    float kv[8], uv[8], av[8];
                     unpack_h8(R.k[q], kv);
                     unpack_h8(R.u[q], uv);
-                    float pk = 0.0f, pq = 0.0f;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const float t = fmaf(kv[j], P[j], 0.0f);
-                        pk = fmaf(t, xk[j], pk);
-                        pq = fmaf(t, xq[j], pq);
-                    }
-                    pk = row16_sum(pk);
-                    pq = row16_sum(pq);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
-                        acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
-                    }
-                    float av[8];
                     unpack_h8(R.a[q], av);
+                    double sk = 0.0;
+                    float sq = 0.0f;
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) P[j] = fmaf(av[j], P[j], 0.0f);
+                    for (int j = 0; j < 8; ++j) {
+                        if (KS) sk = fma((double)kv[j], Yk[j], sk);
+                        sq = fmaf(kv[j], Yq[j], sq);
+                    }
+                    if (KS) sk = row16_sum(sk);
+                    sq = row16_sum(sq);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
+                        acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        if (KS) Yk[j] *= (double)av[j];
+                        Yq[j] *= av[j];
+                    }
                 }
             } else {
                 // scalar decay: one product per slot, applied to the two dot products
-                float P = s_pre0[ts];
+                double P = sh.pre0[ts];
+                float xk[8], xq[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    xk[j] = sh.x[0][SW(l16, j)];
+                    xq[j] = sh.x[1][SW(l16, j)];
+                }
 #pragma unroll
                 for (int q = 0; q < PER_SLOT; ++q) {
                     if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
                     float kv[8], uv[8];
                     unpack_h8(R.k[q], kv);
                     unpack_h8(R.u[q], uv);
-                    float pk = 0.0f, pq = 0.0f;
+                    double sk = 0.0;
+                    float sq = 0.0f;
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        pk = fmaf(kv[j], xk[j], pk);
-                        pq = fmaf(kv[j], xq[j], pq);
+                        if (KS) sk = fma((double)kv[j], (double)xk[j], sk);
+                        sq = fmaf(kv[j], xq[j], sq);
                     }
-                    pk = row16_sum(pk) * P;
-                    pq = row16_sum(pq) * P;
+                    if (KS) sk = row16_sum(sk) * P;
+                    sq = row16_sum(sq) * (float)P;
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
-                        acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+                        if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
+                        acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
                     }
-                    P *= h2f((uint16_t)R.as[q]);
+                    P *= (double)h2f((uint16_t)R.as[q]);
                 }
             }
             if (lo == 0) break;
-            // older records: another pass (scalar gate with W > 64 only).  The
-            // next pass's first barrier orders these scan reads before its writes.
+            // older records: another pass.  The next pass's first barrier orders
+            // these scan reads before its writes.
             hi = lo;
             lo = hi > PASS ? hi - PASS : 0;
             load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
@@ -434,66 +641,9 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
 
     // ---- base and token read vectors (written with the last scan when n > 0) -----
     if (n == 0) {
-        if (tid < D) write_base_vectors(carry, kx, qx, cs, s_y, s_wb, tid);
+        if (tid < D) base_vectors<CODE, KS>(sh, carry, kx, qx, cs, tid);
         wait_vm_all();
         __syncthreads();
-    }
-
-    // ---- quantized residual on the matrix cores ----------------------------------
-    // Per 16-row block of wave w's 32 rows: D (16 rows x 16 columns) = A (rows x
-    // 32 channels of codes, in bf16: every code is a small exact value) times B
-    // (32 channels x columns; column j reads vector j & 1, only columns 0 (k_t)
-    // and 1 (q_t) are kept), with the three bf16 parts of w stacked along the
-    // contraction so the matrix core adds them; fp32 accumulation.  Lane (i, g)
-    // of an operand holds row / column i and 8 channels of group g; the channel
-    // order inside the contraction is free as long as A and B agree: lane g's
-    // 16-code segment s = 4p + g supplies its 8 channels of virtual block 2p
-    // (codes 16s..16s+7) and 2p + 1 (16s+8..16s+15).
-    {
-        typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-        typedef float f32x4 __attribute__((ext_vector_type(4)));
-        const int lane = tid & 63, i16 = lane & 15, g = lane >> 4, wv = tid >> 6;
-        // one accumulator per row block and part: dependent chains of 4
-        f32x4 acc[2][3];
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int part = 0; part < 3; ++part) acc[rb][part] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
-            const int seg = 4 * pp + g;
-            bf16x8 bw[2][3];
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-#pragma unroll
-                for (int part = 0; part < 3; ++part)
-                    bw[h][part] = *(const bf16x8 *)&s_wb[part][i16 & 1][16 * seg + 8 * h];
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                float f[16];
-                decode16<CODE>(lds_codes16<CODE>(s_codes, 32 * wv + 16 * rb + i16, seg), f);
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    uint32_t av[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) av[e] = pack_bf16x2(f[8 * h + 2 * e], f[8 * h + 2 * e + 1]);
-                    const bf16x8 A8 = __builtin_bit_cast(bf16x8, make_uint4(av[0], av[1], av[2], av[3]));
-#pragma unroll
-                    for (int part = 0; part < 3; ++part)
-                        acc[rb][part] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A8, bw[h][part], acc[rb][part], 0, 0, 0);
-                }
-            }
-        }
-        // column i16 (< 2), rows 4 g + r of each block
-        if (i16 < 2) {
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int vrow = 32 * wv + 16 * rb + 4 * g + r;
-                    s_z[i16][POS(vrow)] = s_dlt[vrow] * ((acc[rb][0][r] + acc[rb][1][r]) + acc[rb][2][r]);
-                }
-        }
     }
 
     // ---- Compensator Tokens: token ts, same decay as the base -------------------
@@ -501,30 +651,54 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
         float kv[8], uv[8];
         unpack_h8(ck, kv);
         unpack_h8(cu, uv);
-        float pk = 0.0f, pq = 0.0f;
+        double sk = 0.0;
+        float sq = 0.0f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            pk = fmaf(kv[j], s_y[0][SW(l16, j)], pk);
-            pq = fmaf(kv[j], s_y[1][SW(l16, j)], pq);
+            if (KS) sk = fma((double)kv[j], sh.yk[SW(l16, j)], sk);
+            sq = fmaf(kv[j], sh.yq[SW(l16, j)], sq);
         }
-        pk = row16_sum(pk);
-        pq = row16_sum(pq);
+        if (KS) sk = row16_sum(sk);
+        sq = row16_sum(sq);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            acc_k[j] = fmaf(pk, uv[j], acc_k[j]);
-            acc_q[j] = fmaf(pq, uv[j], acc_q[j]);
+            if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
+            acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
         }
     }
+
+    // ---- quantized residual: thread (v, h) takes half h of code row v -------------
+    {
+        const int v = tid >> 1, h = tid & 1;
+        double zk;
+        float zq;
+        code_product<CODE, KS>(sh, v, h, zk, zq);
+        if (KS) zk += dpp<DPP_XOR1>(zk);
+        zq += dpp<DPP_XOR1>(zq);
+        if (h == 0) {
+            const float dl = sh.dlt[v];
+            if (KS) sh.zk[POS(v)] = (double)dl * zk;
+            sh.zq[POS(v)] = dl * zq;
+        }
+    }
+
     // sum over the wave's 4 slots in registers, then over the 4 waves in LDS:
     // lane (rho, l16) holds channels 8 l16 + 2 rho + e, e = 0, 1, stored at
-    // [2 lane + e]
+    // [2 lane + e] of the wave's rows of the decay array (read only by its own
+    // slots, all of which are past that read)
     {
-        float k0, k1, q0, q1;
-        rows4_reduce_scatter(acc_k, k0, k1);
-        rows4_reduce_scatter(acc_q, q0, q1);
         const int w = tid >> 6, lane = tid & 63;
-        *(float2 *)&s_red[w][0][2 * lane] = make_float2(k0, k1);
-        *(float2 *)&s_red[w][1][2 * lane] = make_float2(q0, q1);
+        double *red_k = &sh.bp[4 * w][0];
+        float *red_q = (float *)(red_k + D);
+        if (KS) {
+            double k0, k1;
+            rows4_reduce_scatter(acc_k, k0, k1);
+            red_k[2 * lane] = k0;
+            red_k[2 * lane + 1] = k1;
+        }
+        float q0, q1;
+        rows4_reduce_scatter(acc_q, q0, q1);
+        *(float2 *)&red_q[2 * lane] = make_float2(q0, q1);
     }
     __syncthreads();
 
@@ -533,18 +707,20 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
         // position t holds channel 8 (t & 15) + (t >> 4) = 8 l16 + 2 rho + e
         const int j = tid >> 4, e = j & 1;
         const int idx = 2 * (16 * (j >> 1) + (tid & 15)) + e;
-        float ak = s_z[0][tid], aq = s_z[1][tid];
+        double ak = KS ? sh.zk[tid] : 0.0;
+        float aq = sh.zq[tid];
 #pragma unroll
         for (int w = 0; w < NT / 64; ++w) {
-            ak += s_red[w][0][idx];
-            aq += s_red[w][1][idx];
+            const double *red_k = &sh.bp[4 * w][0];
+            if (KS) ak += red_k[idx];
+            aq += ((const float *)(red_k + D))[idx];
         }
-        // u_t = fp16(v_t - A^T k_t) (general rule: v_t - S_{i-1}^T b_t); the
-        // b_t = 0 rule reads nothing (the k-side readouts above are then dead
-        // code and compiled out)
-        const uint16_t uh = f2h(RULE == LQ_RULE_ADD ? vx : vx - ak);
+        // u_t = fp16(v_t - A^T k_t) (general rule: v_t - S_{i-1}^T b_t), the
+        // difference rounded to fp32 and then to FP16; the b_t = 0 rule reads
+        // nothing (the k-side readouts above are then dead code and compiled out)
+        const uint16_t uh = RULE == LQ_RULE_ADD ? f2h(vx) : d2h_via_f32((double)vx - ak);
         a.rec_u[(rbase + n) * D + ch] = uh;
-        a.o[tvec + ch] = fmaf(h2f(uh), s_kq[0] + s_kq[1], aq);
+        a.o[tvec + ch] = fmaf(h2f(uh), sh.kq[0] + sh.kq[1], aq);
         if (tid == 0) a.rec_len[tile] = n + 1;
     }
 }

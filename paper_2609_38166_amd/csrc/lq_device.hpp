@@ -88,6 +88,16 @@ __device__ __forceinline__ uint16_t f2h(float f) {      // round to nearest even
 }
 __device__ __forceinline__ float f16_round(float f) { return h2f(f2h(f)); }
 
+// fp16 of the fp32 product a * b: two roundings as written.  Without the empty
+// asm the compiler emits one mixed-precision multiply (v_fma_mixlo_f16) that
+// rounds the exact product straight to FP16, which decides some values
+// differently.
+__device__ __forceinline__ uint16_t f2h_mul(float a, float b) {
+    float p = a * b;
+    asm volatile("" : "+v"(p));
+    return f2h(p);
+}
+
 // fp64 -> fp32 -> fp16, two roundings as written.  The empty asm keeps the
 // compiler from fusing the two conversions into one direct fp64 -> fp16
 // rounding, which decides ties differently.

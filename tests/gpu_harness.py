@@ -279,9 +279,8 @@ def window_sync_parity(wl: synth.Workload, n_windows=None, check=True):
                  records are compared with the oracle's;
       commit  -- teacher-forced: the GPU commits the oracle's window-start
                  representation plus the oracle's records (the gate on codes);
-      chained -- the GPU commits its own records from the decode pass
-                 (reported; any record that differs in its last FP16 bit is
-                 a legitimately different input to the refit).
+      chained -- the GPU commits its own records from the decode pass (the
+                 path the library runs), gated at the same bars.
     Nothing from the GPU is handed to the oracle.
     """
     cfg = ocfg(wl)
@@ -341,9 +340,9 @@ def window_protocol(name, cfg, dims, ref, T, decode, check=True, sample=None, fi
         agg["u_eq"].append(np.mean(ru == eu))
         agg["k_eq"].append(np.mean(rk == ek))
         agg["a_eq"].append(np.mean(ra == ea))
-        # a record that rounds differently may differ by one unit in its last place,
-        # or (near zero) by an fp32-accumulation-sized amount: judge it as a vector
-        agg["rec_ulp"] = max(agg["rec_ulp"], int(_f16_ulp_dist(rk, ek).max()))
+        # a record that rounds differently may differ by one unit in its last place
+        agg["rec_ulp"] = max(agg["rec_ulp"], int(_f16_ulp_dist(rk, ek).max()),
+                             int(_f16_ulp_dist(ru, eu).max()))
         agg["u_rel"] = max(agg["u_rel"], rel_rows(f16_vals(ru), ref["hist_u"][:, sl]))
         # chained commit of the GPU's own records (every tile)
         B.leapquant_window_commit(dims, st, None)
@@ -384,16 +383,15 @@ def window_protocol(name, cfg, dims, ref, T, decode, check=True, sample=None, fi
         assert bits == 0, summary
         assert summary["o_rel"] <= 1e-3, summary
         assert summary["a_eq"] == 1.0 and summary["k_eq"] >= 0.999, summary
-        assert summary["u_eq"] >= 0.995 and summary["u_rel"] <= 1e-3, summary
+        assert summary["u_eq"] >= 0.999 and summary["u_rel"] <= 1e-3, summary
         assert summary["rec_ulp"] <= 1, summary
         assert summary["tf_code_eq"] >= 0.999 and summary["tf_code_maxdiff"] <= 1, summary
         assert summary["tf_deq_rel"] <= 1e-3 and summary["tf_comp_rel"] <= 1e-3, summary
         assert summary["tf_delta_rel"] <= 1e-5 and summary["tf_c_rel"] <= 1e-5, summary
-        # chained commit: two quantizations of states that differ by last-bit FP16
-        # record differences; they must agree to within the method's own
-        # quantization error (the refit may legitimately move between
-        # near-degenerate directions, so codes are reported, not gated)
-        assert summary["ch_ratio"] <= 2.0 and summary["ch_code_eq"] >= 0.95, summary
+        # chained commit (the product path: the GPU commits its own records) at
+        # the same bars as the teacher-forced one
+        assert summary["ch_code_eq"] >= 0.999 and summary["ch_code_maxdiff"] <= 1, summary
+        assert summary["ch_deq_rel"] <= 1e-3 and summary["ch_comp_rel"] <= 1e-3, summary
     return summary
 
 

@@ -214,47 +214,48 @@ def test_window_synchronised_parity(name):
 
 
 def test_free_running_tiny():
-    """The whole GDN tiny trajectory on the GPU alone (its own fp32 prefill, its own
-    quantization, 256 decode steps, 16 commits).  Properties: the GPU's error
-    against the unquantized fp32 trajectory matches the oracle's, and both
-    quantized trajectories agree to well within that error."""
+    """The whole GDN tiny trajectory on the GPU alone: from the oracle's fp32
+    initial state, its own quantization, 256 decode steps and 16 commits of its
+    own records, with nothing handed back from the oracle.  Every output and
+    every window-end representation is held to the bars (outputs and
+    dequantized states within 1e-3, codes equal in >= 99.9 % and at most one
+    step apart).  The quantized trajectory's distance from the unquantized fp32
+    one is reported beside the oracle's."""
     wl = W_["gdn_tiny"]
     H.log("free-running gdn_tiny")
     cfg = H.ocfg(wl)
     S0 = H.oracle_prefill_state(wl)
     streams, tok = H.decode_tokens(wl)
     otok = synth.tile_major(wl, streams, tok)
-    ref = O.run_dense(cfg, S0, otok, snapshots=False)
+    ref = O.run_dense(cfg, S0, otok, snapshots=True)
     o_fp, _ = O.run_baseline(cfg, S0, otok, mode=O.STATE_F32)
-    # GPU: prefill with its own fp32 baseline kernel, outliers, quantize, decode
     dims = H.gdims(wl)
-    pst = synth.Streams(wl, synth.PHASE_PREFILL)
-    ptok = pst.draw(wl.prefill)
-    pdt = H.DeviceTokens(wl, ptok)
-    S_g = torch.zeros((wl.tiles, 128, 128), dtype=torch.float32, device="cuda")
-    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
-    for t in range(wl.prefill):
-        B.leapquant_baseline_step(dims, S_g, B.LQ_STATE_F32, *pdt.step(t), o)
-    F = synth.outlier_factor(synth.outliers(wl))
-    S_g *= H.dev(np.ascontiguousarray(F.transpose(0, 2, 1)))
     st = B.State.empty(dims)
-    B.leapquant_quantize_state(dims, S_g, st)
+    B.leapquant_quantize_state(dims, H.dev(S0.transpose(0, 2, 1).astype(np.float32)), st)
     dt = H.DeviceTokens(wl, tok)
-    outs = []
+    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+    outs, worst = [], {"code_eq": 1.0, "code_maxdiff": 0, "deq_rel": 0.0, "comp_rel": 0.0}
     for t in range(wl.steps):
         B.leapquant_decode_step(dims, st, *dt.step(t), o)
         outs.append(o.cpu().numpy())
         if (t + 1) % wl.window == 0:
             B.leapquant_window_commit(dims, st)
+            w = (t + 1) // wl.window
+            exp = {k_: ref[k_][:, w] for k_ in ("Z", "delta", "c", "Kt", "Ut")}
+            cr = H.compare_rep(cfg, H.download_rep(st), exp, wl.code)
+            worst["code_eq"] = min(worst["code_eq"], cr["code_eq"])
+            for k_ in ("code_maxdiff", "deq_rel", "comp_rel"):
+                worst[k_] = max(worst[k_], cr.get(k_, 0))
     og = np.stack(outs, axis=1)
     assert np.all(np.isfinite(og))
     assert B.leapquant_check_error(st) == 0
-    e_gpu = H.rel(og, o_fp)
-    e_orc = H.rel(ref["o"], o_fp)
-    d = H.rel(og, ref["o"])
-    H.log(f"free-running: gpu-vs-fp32 {e_gpu:.3e} oracle-vs-fp32 {e_orc:.3e} gpu-vs-oracle {d:.3e}")
-    assert 0.5 < e_gpu / e_orc < 2.0
-    assert d < max(2.0 * e_orc, 1e-3)
+    o_rel = H.rel_rows(og, ref["o"])
+    e_gpu, e_orc = H.rel(og, o_fp), H.rel(ref["o"], o_fp)
+    H.log(f"free-running: o_rel {o_rel:.3e} worst commit {worst}; "
+          f"gpu-vs-fp32 {e_gpu:.3e} oracle-vs-fp32 {e_orc:.3e}")
+    assert o_rel <= 1e-3
+    assert worst["code_eq"] >= 0.999 and worst["code_maxdiff"] <= 1, worst
+    assert worst["deq_rel"] <= 1e-3 and worst["comp_rel"] <= 1e-3, worst
 
 
 def test_partial_windows_mask_and_reset():
@@ -296,7 +297,8 @@ def test_partial_windows_mask_and_reset():
     got = {k_: after[k_][:h] for k_ in ("Z", "delta", "c", "Kt", "Ut")}
     cr = H.compare_rep(cfg, got, exp, wl.code)
     H.log("partial chained", cr)
-    assert cr["code_eq"] >= 0.99 and cr["deq_rel"] <= 1e-2, cr
+    assert cr["code_eq"] >= 0.999 and cr["code_maxdiff"] <= 1 and cr["deq_rel"] <= 1e-3, cr
+    assert cr.get("comp_rel", 0.0) <= 1e-3, cr
     # the same partial commit from the oracle's records is exact
     st2 = B.State.empty(dims)
     H.upload_rep(st2, np.arange(wl.tiles), rep0["Z"][:, 0], rep0["delta"][:, 0], rep0["c"][:, 0],
@@ -393,7 +395,7 @@ def test_requests_at_different_window_positions_in_one_launch(name):
     assert np.all(np.isfinite(og)) and o_rel <= 1e-3
     assert np.array_equal(ra, ea)
     assert np.mean(rk == ek) >= 0.999 and int(H._f16_ulp_dist(rk, ek).max()) <= 1
-    assert np.mean(ru == eu) >= 0.995 and u_rel <= 1e-3
+    assert np.mean(ru == eu) >= 0.999 and int(H._f16_ulp_dist(ru, eu).max()) <= 1 and u_rel <= 1e-3
     # commit of the partial windows, from the oracle's records
     p_t = n_t + 1
     st2 = B.State.empty(dims)
