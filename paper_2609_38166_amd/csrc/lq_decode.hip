@@ -163,21 +163,22 @@ __device__ __forceinline__ void rows4_reduce_scatter(const double *x, double &s0
     s1 = a + b;
 }
 
-// Largest value of x over the 64 lanes of the wave (uniform result).
+// Largest value of x over the 64 lanes of the wave (every lane gets it).
 __device__ __forceinline__ int wave_max_i32(int x) {
     x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_XOR1, 0xF, 0xF, false));
     x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_XOR2, 0xF, 0xF, false));
     x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_ROR4, 0xF, 0xF, false));
     x = max(x, __builtin_amdgcn_update_dpp(0, x, DPP_ROR8, 0xF, 0xF, false));
-    const int a = max(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16));
-    const int b = max(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48));
-    return max(a, b);
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);     // rows rho, rho ^ 2
+    x = max((int)r[0], (int)r[1]);
+    const auto r2 = __builtin_amdgcn_permlane16_swap(x, x, false, false);    // rows rho, rho ^ 1
+    return max((int)r2[0], (int)r2[1]);
 }
 
 // Code rows in LDS are stored in 16-byte chunks, each row rotated by zrot(v)
-// chunks, so that the lanes of a code-product read (consecutive rows, two
-// halves of each) fall in distinct banks.  The rotation is applied when the
-// copy is issued (lane L's destination is fixed; its source chunk is
+// chunks, so that the lanes of one matrix-core operand read (16 consecutive
+// rows at one chunk position) fall in distinct banks.  The rotation is applied
+// when the copy is issued (lane L's destination is fixed; its source chunk is
 // chosen).  The 6-bit rows (96 bytes) are not rotated.
 template <int CODE> struct Rows {
     static constexpr int BYTES = D * CodeFmt<CODE>::BITS / 8;
@@ -290,111 +291,123 @@ __device__ __forceinline__ void base_vectors(DecodeShared<CODE> &sh, double G, f
     }
 }
 
-// Code product of one half row: thread (v, h) sums over channels 64h .. 64h+63
-// of row v.  Integer codes: per digit and per exponent group (g = (c >> 2) & 1,
-// the scan wave that set the exponent) an exact int32 sum of int8 products.
+// E4M3 code product of one half row: thread (v, h) sums over channels
+// 64h .. 64h+63 of row v, k side in fp64, q side in fp32 (E4M3 codes are not
+// integers, so the digit product below does not apply).
 template <int CODE, bool KS>
-__device__ __forceinline__ void code_product(const DecodeShared<CODE> &sh, int v, int h, double &zk, float &zq) {
-    if (CODE == 1) {
-        const double *wkv = (const double *)sh.rv;
-        const float *wqv = (const float *)(sh.rv + D * 8);
-        double sk = 0.0;
-        float sq = 0.0f;
-#pragma unroll 1
-        for (int m = 0; m < 4; ++m) {
-            const int c = 4 * h + m;
-            const uint4 z = lds_chunk<CODE>(sh.codes, v, c);
-            const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const int c0 = 16 * c + 4 * p;         // channels c0 .. c0 + 3
-                const float4 wq = *(const float4 *)&wqv[c0];
-                const float f0 = e4m3_to_f<0>(zw[p]), f1 = e4m3_to_f<1>(zw[p]);
-                const float f2 = e4m3_to_f<2>(zw[p]), f3 = e4m3_to_f<3>(zw[p]);
-                sq = fmaf(f0, wq.x, sq);
-                sq = fmaf(f1, wq.y, sq);
-                sq = fmaf(f2, wq.z, sq);
-                sq = fmaf(f3, wq.w, sq);
-                if (KS) {
-                    const double2 wa = *(const double2 *)&wkv[c0], wb = *(const double2 *)&wkv[c0 + 2];
-                    sk = fma((double)f0, wa.x, sk);
-                    sk = fma((double)f1, wa.y, sk);
-                    sk = fma((double)f2, wb.x, sk);
-                    sk = fma((double)f3, wb.y, sk);
-                }
-            }
-        }
-        zk = sk;
-        zq = sq;
-        return;
-    }
-    constexpr int D0 = KS ? 0 : KDIG;            // first digit row used
-    const uint32_t *dig = (const uint32_t *)sh.rv;   // [NDIG][D / 4] words
-    int acc[NDIG][2];
-#pragma unroll
-    for (int d = 0; d < NDIG; ++d) acc[d][0] = acc[d][1] = 0;
-    // the 4-channel words of this half row as int8 bytes: word i holds
-    // channels 64h + 4i .. 64h + 4i + 3, exponent group i & 1
-    auto dot_word = [&](uint32_t zb, int i) {
-        const int g = i & 1;
-#pragma unroll
-        for (int d = D0; d < NDIG; ++d)
-            acc[d][g] = __builtin_amdgcn_sdot4((int)zb, (int)dig[d * (D / 4) + 16 * h + i], acc[d][g], false);
-    };
-    if (CODE == 0) {
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const uint4 z = lds_chunk<CODE>(sh.codes, v, 4 * h + m);
-            dot_word(z.x, 4 * m + 0);
-            dot_word(z.y, 4 * m + 1);
-            dot_word(z.z, 4 * m + 2);
-            dot_word(z.w, 4 * m + 3);
-        }
-    } else if (CODE == 2) {
-        // 32 codes per chunk, two chunks per half row; each word holds 8 channels
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const uint4 z = lds_chunk<CODE>(sh.codes, v, 2 * h + m);
-            const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                dot_word(int4x4_to_bytes(zw[p], 0), 8 * m + 2 * p);
-                dot_word(int4x4_to_bytes(zw[p], 1), 8 * m + 2 * p + 1);
-            }
-        }
-    } else {
-        // 48 bytes per half row, four units of 12 bytes = 4 groups of 3 bytes
-        const uint32_t *zr = (const uint32_t *)sh.codes + v * (Rows<CODE>::BYTES / 4) + 12 * h;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t w0 = zr[3 * u], w1 = zr[3 * u + 1], w2 = zr[3 * u + 2];
-            dot_word(int6x4_to_bytes(w0 & 0xFFFFFFu), 4 * u);
-            dot_word(int6x4_to_bytes(__builtin_amdgcn_alignbit(w1, w0, 24) & 0xFFFFFFu), 4 * u + 1);
-            dot_word(int6x4_to_bytes(__builtin_amdgcn_alignbit(w2, w1, 16) & 0xFFFFFFu), 4 * u + 2);
-            dot_word(int6x4_to_bytes(w2 >> 8), 4 * u + 3);
-        }
-    }
-    // sum_d acc_d 128^-d is exact in fp64 (|acc_d| < 2^19, 34 bits below)
+__device__ __forceinline__ void code_product_e4m3(const DecodeShared<CODE> &sh, int v, int h, double &zk,
+                                                  float &zq) {
+    const double *wkv = (const double *)sh.rv;
+    const float *wqv = (const float *)(sh.rv + D * 8);
     double sk = 0.0;
-    if (KS) {
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-            double s = (double)acc[KDIG - 1][g];
-#pragma unroll
-            for (int d = KDIG - 2; d >= 0; --d) s = fma(s, 0x1p-7, (double)acc[d][g]);
-            sk += __builtin_ldexp(s, sh.ex[0][g] - 6);
-        }
-    }
     float sq = 0.0f;
+#pragma unroll 1
+    for (int m = 0; m < 4; ++m) {
+        const int c = 4 * h + m;
+        const uint4 z = lds_chunk<CODE>(sh.codes, v, c);
+        const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-        float s = (float)acc[NDIG - 1][g];
-#pragma unroll
-        for (int d = NDIG - 2; d >= KDIG; --d) s = fmaf(s, 0x1p-7f, (float)acc[d][g]);
-        sq += __builtin_ldexpf(s, sh.ex[1][g] - 6);
+        for (int p = 0; p < 4; ++p) {
+            const int c0 = 16 * c + 4 * p;         // channels c0 .. c0 + 3
+            const float4 wq = *(const float4 *)&wqv[c0];
+            const float f0 = e4m3_to_f<0>(zw[p]), f1 = e4m3_to_f<1>(zw[p]);
+            const float f2 = e4m3_to_f<2>(zw[p]), f3 = e4m3_to_f<3>(zw[p]);
+            sq = fmaf(f0, wq.x, sq);
+            sq = fmaf(f1, wq.y, sq);
+            sq = fmaf(f2, wq.z, sq);
+            sq = fmaf(f3, wq.w, sq);
+            if (KS) {
+                const double2 wa = *(const double2 *)&wkv[c0], wb = *(const double2 *)&wkv[c0 + 2];
+                sk = fma((double)f0, wa.x, sk);
+                sk = fma((double)f1, wa.y, sk);
+                sk = fma((double)f2, wb.x, sk);
+                sk = fma((double)f3, wb.y, sk);
+            }
+        }
     }
     zk = sk;
     zq = sq;
+}
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Codes of channels c0 .. c0 + 15 of row v as sixteen int8 bytes, in channel
+// order (c0 a multiple of 16).
+template <int CODE>
+__device__ __forceinline__ v4i codes_i8(const DecodeShared<CODE> &sh, int v, int c0) {
+    if (CODE == 0) {
+        const uint4 z = lds_chunk<CODE>(sh.codes, v, c0 >> 4);
+        return v4i{(int)z.x, (int)z.y, (int)z.z, (int)z.w};
+    }
+    if (CODE == 2) {                                     // 32 codes per chunk
+        const uint4 z = lds_chunk<CODE>(sh.codes, v, c0 >> 5);
+        const uint32_t w0 = (c0 & 16) ? z.z : z.x, w1 = (c0 & 16) ? z.w : z.y;
+        return v4i{(int)int4x4_to_bytes(w0, 0), (int)int4x4_to_bytes(w0, 1), (int)int4x4_to_bytes(w1, 0),
+                   (int)int4x4_to_bytes(w1, 1)};
+    }
+    // 6-bit rows are not rotated; channels c0 .. c0 + 15 are 12 bytes at 3 c0 / 4
+    const uint32_t *zr = (const uint32_t *)sh.codes + v * (Rows<CODE>::BYTES / 4) + 3 * (c0 >> 4);
+    const uint32_t w0 = zr[0], w1 = zr[1], w2 = zr[2];
+    return v4i{(int)int6x4_to_bytes(w0 & 0xFFFFFFu),
+               (int)int6x4_to_bytes(__builtin_amdgcn_alignbit(w1, w0, 24) & 0xFFFFFFu),
+               (int)int6x4_to_bytes(__builtin_amdgcn_alignbit(w2, w1, 16) & 0xFFFFFFu),
+               (int)int6x4_to_bytes(w2 >> 8)};
+}
+
+// Integer code product of wave w's 32 rows on the integer matrix cores.  The
+// products are exact: every code and every digit is an int8, and the int32
+// sums are exact.  Column n of the 16 x 16 x 64 product is digit d = n & 7 of
+// exponent group g = n >> 3 (the channels of the other group contribute 0),
+// so one v_mfma_i32_16x16x64_i8 per 16 rows and 64 channels gives every
+// digit sum at once.  The digit sums pass through the wave's own rows
+// 4w+2 .. 4w+3 of the decay array (a 16 x 32 int32 transpose), and lane
+// (side, r) combines row 32w + r: side 0 the k digits in fp64 (exactly, the
+// sums being below 2^19 and 34 bits deep), side 1 the q digits in fp32.
+template <int CODE, bool KS>
+__device__ __forceinline__ void code_product_mfma(DecodeShared<CODE> &sh, int tid) {
+    const int lane = tid & 63, w = tid >> 6, i16 = lane & 15, kb = lane >> 4;
+    const int d = i16 & 7, g = i16 >> 3;
+    v4i acc[2] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const int c0 = 64 * s + 16 * kb;                 // this lane's 16 channels
+        const uint4 bq = *(const uint4 *)(sh.rv + d * D + c0);
+        // words 0 and 2 hold exponent group 0 (channels c with (c >> 2) & 1 = 0)
+        const v4i b = {g ? 0 : (int)bq.x, g ? (int)bq.y : 0, g ? 0 : (int)bq.z, g ? (int)bq.w : 0};
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+            acc[rb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(codes_i8<CODE>(sh, 32 * w + 16 * rb + i16, c0), b,
+                                                           acc[rb], 0, 0, 0);
+    }
+    // lane (kb, i16) holds rows 16 rb + 4 kb + 0..3 of column i16
+    int *T = (int *)&sh.bp[4 * w + 2][0];                // [16 columns][32 rows]
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) *(v4i *)&T[i16 * 32 + 16 * rb + 4 * kb] = acc[rb];
+    const int r = lane & 31, v = 32 * w + r;
+    const float dl = sh.dlt[v];
+    if (lane < 32) {
+        if (KS) {
+            double zk = 0.0;
+#pragma unroll
+            for (int gg = 0; gg < 2; ++gg) {
+                double t = (double)T[(8 * gg + KDIG - 1) * 32 + r];
+#pragma unroll
+                for (int dd = KDIG - 2; dd >= 0; --dd) t = fma(t, 0x1p-7, (double)T[(8 * gg + dd) * 32 + r]);
+                zk += __builtin_ldexp(t, sh.ex[0][gg] - 6);
+            }
+            sh.zk[POS(v)] = (double)dl * zk;
+        }
+    } else {
+        float zq = 0.0f;
+#pragma unroll
+        for (int gg = 0; gg < 2; ++gg) {
+            float t = (float)T[(8 * gg + NDIG - 1) * 32 + r];
+#pragma unroll
+            for (int dd = NDIG - 2; dd >= KDIG; --dd) t = fmaf(t, 0x1p-7f, (float)T[(8 * gg + dd) * 32 + r]);
+            zq += __builtin_ldexpf(t, sh.ex[1][gg] - 6);
+        }
+        sh.zq[POS(v)] = dl * zq;
+    }
 }
 
 template <int GATE, int CODE, int RULE>
@@ -481,9 +494,8 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
     if (RULE == LQ_RULE_GENERAL) asm volatile("" : "+v"(bx));
 
     // ---- token inputs, this token's record -------------------------------------
-    // carry: decay of every record newer than the current pass, channel ch
-    // (the scalar gate keeps the same product in every thread below D)
-    double carry = 1.0;
+    // carry0: this token's FP16 decay (1 under the general rule), exact in fp32
+    float carry0 = 1.0f;
     if (tid < D) {
         const uint16_t ah = f2h(al);
         // read vectors: k_t and q_t under the decay of this token (carry), or
@@ -492,7 +504,7 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
         const float xk = gen ? bx : kx, xq = gen ? h2f(ah) * qx : qx;
         sh.x[0][tid] = xk;
         sh.x[1][tid] = xq;
-        if (!gen) carry = (double)h2f(ah);
+        if (!gen) carry0 = h2f(ah);
         const size_t slot = rbase + n;
         if (GATE) a.rec_a[slot * D + ch] = ah;
         else if (tid == 0) a.rec_a[slot] = ah;
@@ -504,146 +516,172 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
         qx = xq;
     }
 
+    // partial readouts of this thread's slot, k side and q side (defined after
+    // the first scan, so that they hold no registers before it)
     double acc_k[8];
     float acc_q[8];
+
+    // decay product of this slot's block, per channel of its segment (up to
+    // three FP16 factors: exact in fp64)
+    auto block_products = [&]() {
+        if (GATE) {
+            double bp[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        acc_k[j] = 0.0;
-        acc_q[j] = 0.0f;
-    }
+            for (int j = 0; j < 8; ++j) bp[j] = 1.0;
+#pragma unroll
+            for (int q = 0; q < PER_SLOT; ++q) {
+                if (hi - 1 - (PER_SLOT * ts + q) >= lo) {
+                    const uint32_t w4[4] = {R.a[q].x, R.a[q].y, R.a[q].z, R.a[q].w};
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) bp[j] *= h2d(w4[j >> 1], j & 1);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sh.bp[ts][SW(l16, j)] = bp[j];
+        } else {
+            double bp = 1.0;
+#pragma unroll
+            for (int q = 0; q < PER_SLOT; ++q)
+                if (hi - 1 - (PER_SLOT * ts + q) >= lo) bp *= (double)h2f((uint16_t)R.as[q]);
+            if (l16 == 0) sh.bp[ts][0] = bp;
+        }
+    };
+    // exclusive scan over the slots (threads t < D); after the last pass the
+    // carry is Gamma_{1:i} and the base read vectors are written
+    // carry: decay of every record newer than the current pass, channel ch
+    // (the scalar gate keeps the same product in every thread below D)
+    double carry = 1.0;
+    auto scan = [&](bool first) {
+        // slot 0 holds the newest block
+        if (tid < D) {
+            double c = first ? (double)carry0 : carry;
+            // slot products read ahead of the chain (eight at a time), then
+            // overwritten
+#pragma unroll
+            for (int s0 = 0; s0 < SLOTS; s0 += 8) {
+                double bv[8];
+#pragma unroll
+                for (int s = 0; s < 8; ++s) bv[s] = sh.bp[s0 + s][GATE ? tid : 0];
+#pragma unroll
+                for (int s = 0; s < 8; ++s) {
+                    if (GATE) sh.bp[s0 + s][tid] = c;
+                    else if (tid == 0) sh.pre0[s0 + s] = c;
+                    c *= bv[s];
+                }
+            }
+            carry = c;
+            if (lo == 0) base_vectors<CODE, KS>(sh, carry, kx, qx, cs, tid);   // carry = Gamma_{1:i}
+        }
+    };
+    // the slot's records, newest first
+    auto walk = [&]() {
+        if (GATE) {
+            // Y = Gamma_{j+1:i} . x for the slot's newest record, then older
+            double Yk[8];
+            float Yq[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const double P = sh.bp[ts][SW(l16, j)];
+                Yk[j] = P * (double)sh.x[0][SW(l16, j)];
+                Yq[j] = (float)P * sh.x[1][SW(l16, j)];
+            }
+#pragma unroll
+            for (int q = 0; q < PER_SLOT; ++q) {
+                if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                float kv[8], uv[8], av[8];
+                unpack_h8(R.k[q], kv);
+                unpack_h8(R.u[q], uv);
+                unpack_h8(R.a[q], av);
+                double sk = 0.0;
+                float sq = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (KS) sk = fma((double)kv[j], Yk[j], sk);
+                    sq = fmaf(kv[j], Yq[j], sq);
+                }
+                if (KS) sk = row16_sum(sk);
+                sq = row16_sum(sq);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
+                    acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (KS) Yk[j] *= (double)av[j];
+                    Yq[j] *= av[j];
+                }
+            }
+        } else {
+            // scalar decay: one product per slot, applied to the two dot products
+            double P = sh.pre0[ts];
+            float xk[8], xq[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                xk[j] = sh.x[0][SW(l16, j)];
+                xq[j] = sh.x[1][SW(l16, j)];
+            }
+#pragma unroll
+            for (int q = 0; q < PER_SLOT; ++q) {
+                if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                float kv[8], uv[8];
+                unpack_h8(R.k[q], kv);
+                unpack_h8(R.u[q], uv);
+                double sk = 0.0;
+                float sq = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (KS) sk = fma((double)kv[j], (double)xk[j], sk);
+                    sq = fmaf(kv[j], xq[j], sq);
+                }
+                if (KS) sk = row16_sum(sk) * P;
+                sq = row16_sum(sq) * (float)P;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
+                    acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
+                }
+                P *= (double)h2f((uint16_t)R.as[q]);
+            }
+        }
+    };
 
     // ---- buffered records, newest first, up to PASS per pass ----------------------
     if (n > 0) {
-        while (true) {
-            // decay product of this slot's block, per channel of its segment
-            // (up to three FP16 factors: exact in fp64)
-            if (GATE) {
-                double bp[8];
+        block_products();
+        __syncthreads();
+        scan(true);
+        if (lo == 0) wait_vm_all();      // this wave's code copies have landed
+        __syncthreads();
 #pragma unroll
-                for (int j = 0; j < 8; ++j) bp[j] = 1.0;
-#pragma unroll
-                for (int q = 0; q < PER_SLOT; ++q) {
-                    if (hi - 1 - (PER_SLOT * ts + q) >= lo) {
-                        const uint32_t w4[4] = {R.a[q].x, R.a[q].y, R.a[q].z, R.a[q].w};
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) bp[j] *= h2d(w4[j >> 1], j & 1);
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) sh.bp[ts][SW(l16, j)] = bp[j];
-            } else {
-                double bp = 1.0;
-#pragma unroll
-                for (int q = 0; q < PER_SLOT; ++q)
-                    if (hi - 1 - (PER_SLOT * ts + q) >= lo) bp *= (double)h2f((uint16_t)R.as[q]);
-                if (l16 == 0) sh.bp[ts][0] = bp;
-            }
-            __syncthreads();
-            // exclusive scan over the slots; slot 0 holds the newest block
-            if (tid < D) {
-                double c = carry;
-                // slot products read ahead of the chain (eight at a time), then
-                // overwritten
-#pragma unroll
-                for (int s0 = 0; s0 < SLOTS; s0 += 8) {
-                    double bv[8];
-#pragma unroll
-                    for (int s = 0; s < 8; ++s) bv[s] = sh.bp[s0 + s][GATE ? tid : 0];
-#pragma unroll
-                    for (int s = 0; s < 8; ++s) {
-                        if (GATE) sh.bp[s0 + s][tid] = c;
-                        else if (tid == 0) sh.pre0[s0 + s] = c;
-                        c *= bv[s];
-                    }
-                }
-                carry = c;
-                if (lo == 0) base_vectors<CODE, KS>(sh, carry, kx, qx, cs, tid);   // carry = Gamma_{1:i}
-            }
-            if (lo == 0) wait_vm_all();  // this wave's code copies have landed
-            __syncthreads();
-            if (GATE) {
-                // Y = Gamma_{j+1:i} . x for the slot's newest record, then older
-                double Yk[8];
-                float Yq[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const double P = sh.bp[ts][SW(l16, j)];
-                    Yk[j] = P * (double)sh.x[0][SW(l16, j)];
-                    Yq[j] = (float)P * sh.x[1][SW(l16, j)];
-                }
-#pragma unroll
-                for (int q = 0; q < PER_SLOT; ++q) {
-                    if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
-                    float kv[8], uv[8], av[8];
-                    unpack_h8(R.k[q], kv);
-                    unpack_h8(R.u[q], uv);
-                    unpack_h8(R.a[q], av);
-                    double sk = 0.0;
-                    float sq = 0.0f;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        if (KS) sk = fma((double)kv[j], Yk[j], sk);
-                        sq = fmaf(kv[j], Yq[j], sq);
-                    }
-                    if (KS) sk = row16_sum(sk);
-                    sq = row16_sum(sq);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
-                        acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
-                    }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        if (KS) Yk[j] *= (double)av[j];
-                        Yq[j] *= av[j];
-                    }
-                }
-            } else {
-                // scalar decay: one product per slot, applied to the two dot products
-                double P = sh.pre0[ts];
-                float xk[8], xq[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    xk[j] = sh.x[0][SW(l16, j)];
-                    xq[j] = sh.x[1][SW(l16, j)];
-                }
-#pragma unroll
-                for (int q = 0; q < PER_SLOT; ++q) {
-                    if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
-                    float kv[8], uv[8];
-                    unpack_h8(R.k[q], kv);
-                    unpack_h8(R.u[q], uv);
-                    double sk = 0.0;
-                    float sq = 0.0f;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        if (KS) sk = fma((double)kv[j], (double)xk[j], sk);
-                        sq = fmaf(kv[j], xq[j], sq);
-                    }
-                    if (KS) sk = row16_sum(sk) * P;
-                    sq = row16_sum(sq) * (float)P;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        if (KS) acc_k[j] = fma(sk, (double)uv[j], acc_k[j]);
-                        acc_q[j] = fmaf(sq, uv[j], acc_q[j]);
-                    }
-                    P *= (double)h2f((uint16_t)R.as[q]);
-                }
-            }
-            if (lo == 0) break;
-            // older records: another pass.  The next pass's first barrier orders
-            // these scan reads before its writes.
+        for (int j = 0; j < 8; ++j) {
+            acc_k[j] = 0.0;
+            acc_q[j] = 0.0f;
+        }
+        walk();
+        while (lo > 0) {
+            // older records: another pass.  Its first barrier orders this pass's
+            // reads of the decay array before the next scan's writes.
             hi = lo;
             lo = hi > PASS ? hi - PASS : 0;
             load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
+            block_products();
+            __syncthreads();
+            scan(false);
+            if (lo == 0) wait_vm_all();
+            __syncthreads();
+            walk();
         }
-    }
-
-    // ---- base and token read vectors (written with the last scan when n > 0) -----
-    if (n == 0) {
-        if (tid < D) base_vectors<CODE, KS>(sh, carry, kx, qx, cs, tid);
+    } else {
+        // ---- no records: base read vectors only ----
+        if (tid < D) base_vectors<CODE, KS>(sh, (double)carry0, kx, qx, cs, tid);
         wait_vm_all();
         __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            acc_k[j] = 0.0;
+            acc_q[j] = 0.0f;
+        }
     }
 
     // ---- Compensator Tokens: token ts, same decay as the base -------------------
@@ -667,12 +705,13 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
         }
     }
 
-    // ---- quantized residual: thread (v, h) takes half h of code row v -------------
-    {
+    // ---- quantized residual -------------------------------------------------------
+    if (CODE == 1) {
+        // thread (v, h) takes half h of code row v
         const int v = tid >> 1, h = tid & 1;
         double zk;
         float zq;
-        code_product<CODE, KS>(sh, v, h, zk, zq);
+        code_product_e4m3<CODE, KS>(sh, v, h, zk, zq);
         if (KS) zk += dpp<DPP_XOR1>(zk);
         zq += dpp<DPP_XOR1>(zq);
         if (h == 0) {
@@ -680,6 +719,8 @@ __global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
             if (KS) sh.zk[POS(v)] = (double)dl * zk;
             sh.zq[POS(v)] = dl * zq;
         }
+    } else {
+        code_product_mfma<CODE, KS>(sh, tid);
     }
 
     // sum over the wave's 4 slots in registers, then over the 4 waves in LDS:
