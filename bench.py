@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--cpu-sample-tiles", type=int, default=8192)
     ap.add_argument("--profile", action="store_true",
                     help="short run for profilers: setup, warmup and the timed steps only")
+    ap.add_argument("--profile-decode", action="store_true",
+                    help="short run for profilers: setup, then the decode with rotating batches (the "
+                         "roofline timing) and one device copy for calibrating byte counters")
     return ap.parse_args()
 
 
@@ -348,16 +351,16 @@ def bulk_quantize(reps=3):
             "note": "fp64 fit, smoothing and codes per state: bound by vector-ALU issue, not by HBM"}
 
 
-def decode_two_batches(wl, dims, S0, toks, reps=3):
-    """Average decode launch duration when two independent batches of the same
-    size alternate launch by launch (positions 1..W each, one graph): the other
-    batch's codes evict this batch's from the 256 MB Infinity Cache, so the
-    codes come from HBM on every step.  In the single-batch loop a batch's
-    int8 codes (134 MB at 8192 tiles) can stay resident from one step to the
-    next; this figure is the decode without that help."""
+def decode_rotating(wl, dims, S0, toks, copies=2, reps=3):
+    """Average decode launch duration when `copies` independent batches of the
+    same size take turns launch by launch (positions 1..W each, one graph), so
+    that between two steps of one batch the others stream through the 256 MB
+    Infinity Cache and evict its state: every step reads its codes from HBM.
+    (In a loop over one batch its codes can stay resident from one step to the
+    next when they fit.)"""
     import torch
     from paper_2609_38166_amd import binding as B_
-    sts = [B_.State.empty(dims) for _ in range(2)]
+    sts = [B_.State.empty(dims) for _ in range(copies)]
     o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
     q, k, v, a, b = toks
     W = wl.window
@@ -389,12 +392,20 @@ def decode_two_batches(wl, dims, S0, toks, reps=3):
         e1.record()
         torch.cuda.synchronize()
         if rep:
-            ts.append(e0.elapsed_time(e1) / (2 * W))
+            ts.append(e0.elapsed_time(e1) / (copies * W))
     for st in sts:
         if B_.leapquant_check_error(st):
-            raise RuntimeError("device error during the two-batch decode timing")
+            raise RuntimeError("device error during the rotating-batch decode timing")
     del sts
     return float(np.mean(ts))
+
+
+def cold_copies(wl):
+    """Batches to rotate so that the others' state (codes, scales, compensators
+    and the window's records) exceeds 512 MB, twice the Infinity Cache."""
+    per = wl.tiles * (code_bytes(wl) + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+                      + wl.window * rec_bytes(wl))
+    return max(2, 1 + int(np.ceil(512e6 / per)))
 
 
 def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3, one_batch=False):
@@ -481,6 +492,163 @@ def staggered_windows(wl, dims, S0, toks, groups=(1, 4), reps=3, one_batch=False
         del g
     del st
     return res
+
+
+def fused_schedules(wl, dims, S0, toks, G=4, reps=3):
+    """The decode step fused with the window-end commit (row f2), per decode step
+    over one window cycle, replayed as one graph each:
+      aligned_unfused -- W decode launches, then a commit of every tile (the
+                         headline schedule);
+      aligned_fused   -- W - 1 decode launches, then one fused launch that
+                         decodes and commits every tile;
+      staggered_fused -- requests in G groups whose windows are offset by W/G
+                         steps; every step is one fused launch, in which the
+                         group whose window fills commits;
+      staggered_unfused -- the same schedule as a decode launch plus a commit
+                         masked to that group.
+    commit_share_aligned is the commit's part of the aligned unfused cycle."""
+    import torch
+    from paper_2609_38166_amd import binding as B_
+    W, Bt = wl.window, wl.batch
+    q, k, v, a, b = toks
+    st = B_.State.empty(dims)
+    o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+    R = Bt // G
+    offs = torch.as_tensor([(bi // R) * W // G for bi in range(Bt)], dtype=torch.int32, device="cuda")
+    masks = []
+    for gi in range(G):
+        mk = torch.zeros(Bt, dtype=torch.int32, device="cuda")
+        mk[gi * R:(gi + 1) * R] = 1
+        masks.append(mk)
+
+    def aligned(fused):
+        def cycle():
+            for t in range(W):
+                if fused and t == W - 1:
+                    B_.leapquant_decode_step_commit(dims, st, q[t], k[t], v[t], a[t], b[t], o)
+                else:
+                    B_.leapquant_decode_step(dims, st, q[t], k[t], v[t], a[t], b[t], o)
+            if not fused:
+                B_.leapquant_window_commit(dims, st)
+        return cycle, False
+
+    def staggered(fused):
+        def cycle():
+            for t in range(W):
+                if fused:
+                    B_.leapquant_decode_step_commit(dims, st, q[t], k[t], v[t], a[t], b[t], o)
+                else:
+                    B_.leapquant_decode_step(dims, st, q[t], k[t], v[t], a[t], b[t], o)
+                    for gi in range(G):
+                        if (t + 1 + gi * W // G) % W == 0:
+                            B_.leapquant_window_commit(dims, st, masks[gi])
+        return cycle, True
+
+    res = {}
+    for name, (cycle, stag) in (("aligned_unfused", aligned(False)), ("aligned_fused", aligned(True)),
+                                ("staggered_unfused", staggered(False)), ("staggered_fused", staggered(True))):
+        def reset():
+            B_.leapquant_quantize_state(dims, S0, st)
+            if stag:
+                st.rec_len.copy_(offs[:, None].expand(Bt, wl.heads_v))
+        reset()
+        cycle()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        reset()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            cycle()
+        ts = []
+        for rep in range(reps + 1):
+            reset()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                ts.append(e0.elapsed_time(e1) / W)
+        if B_.leapquant_check_error(st):
+            raise RuntimeError(f"device error during the {name} schedule")
+        res[f"{name}_us_per_step"] = round(float(np.mean(ts)) * 1e3, 2)
+        del g
+    del st
+    res["groups"] = G
+    return res
+
+
+def device_inputs(wl, T, seed):
+    """Step-major tokens of T steps and an fp32 state drawn on the device with
+    the workload's distributions (unit q and k, v ~ N(0, I), beta = sigmoid(N),
+    decay = exp(-0.1 softplus(N))).  For throughput only: no kernel's work
+    depends on the values."""
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    B_, Hv, Hk = wl.batch, wl.heads_v, wl.heads_k
+
+    def rn(*shape):
+        return torch.randn(shape, generator=g, device="cuda")
+    q, k = rn(T, B_, Hk, wl.dk), rn(T, B_, Hk, wl.dk)
+    q /= q.norm(dim=-1, keepdim=True)
+    k /= k.norm(dim=-1, keepdim=True)
+    v = rn(T, B_, Hv, wl.dv)
+    a = torch.exp(-0.1 * torch.nn.functional.softplus(rn(T, B_, Hv, wl.dk) if wl.g > 1 else rn(T, B_, Hv)))
+    b = torch.sigmoid(rn(T, B_, Hv))
+    S0 = rn(B_, Hv, wl.dv, wl.dk) * 0.1
+    return S0, (q, k, v, a, b)
+
+
+def config_line(wl, args):
+    """Throughput of one more workload shape: kernel times over one window
+    (cache-resident and with rotating batches), token-head steps/s from the
+    kernel times of the whole T-token trace, the decode's roofline, and the
+    per-step bf16 / fp32 baselines at the same shape."""
+    import torch
+    from paper_2609_38166_amd import binding as B_
+    dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=wl.window, n_comp=wl.n_comp,
+                        power_iters=wl.power_iters, gate=wl.gate, code=wl.code)
+    W = wl.window
+    S0, toks = device_inputs(wl, W, wl.seed + 17)
+    kt = per_launch_times(wl, dims, S0, toks)
+    ncold = cold_copies(wl)
+    cold = decode_rotating(wl, dims, S0, toks, copies=ncold)
+    dbytes = float(np.mean([decode_bytes(wl, i) for i in range(1, W + 1)])) * wl.tiles
+    step_ms = cold + kt["commit_ms"] / W                      # per token, commits amortised
+    trace_ms = cold * wl.steps + kt["commit_ms"] * (wl.steps // W) + kt["quantize_ms"]
+    q, k, v, a, b = toks
+    base = {}
+    for name, dtype, tdt in (("bf16", B_.LQ_STATE_BF16, torch.bfloat16), ("fp32", B_.LQ_STATE_F32, torch.float32)):
+        S = S0.to(tdt).contiguous()
+        o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+
+        def run(S=S, o=o, dtype=dtype):
+            for t in range(W):
+                B_.leapquant_baseline_step(dims, S, dtype, q[t], k[t], v[t], a[t], b[t], o)
+        run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run()
+        bs, _ = time_steps(g.replay, 2, 1)
+        base[name] = bs / (2 * W) * 1e3
+        del S, g
+    out = {"workload": wl.name, "tiles": wl.tiles, "heads_k": wl.heads_k, "tokens": wl.steps, "window": W,
+           "n_comp": wl.n_comp, "code": {0: "int8", 1: "e4m3", 2: "int4", 3: "int6"}[wl.code],
+           "value": round(wl.tiles * wl.steps / (trace_ms * 1e-3), 1), "unit": "token-head steps/s",
+           "ms_per_trace_from_kernels": round(trace_ms, 3),
+           "decode_us": round(cold * 1e3, 2), "decode_us_cache_resident": round(kt["decode_ms"] * 1e3, 2),
+           "commit_us": round(kt["commit_ms"] * 1e3, 2), "quantize_us": round(kt["quantize_ms"] * 1e3, 2),
+           "roofline": {"kernel": "decode_step", "bound": "hbm",
+                        "achieved": round(dbytes / (cold * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(dbytes / (cold * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                        "bytes_per_launch": round(dbytes), "rotating_batches": ncold},
+           "bf16_us_per_step": round(base["bf16"] * 1e3, 2), "fp32_us_per_step": round(base["fp32"] * 1e3, 2),
+           "speedup_vs_bf16": round(base["bf16"] / step_ms, 3), "speedup_vs_fp32": round(base["fp32"] / step_ms, 3),
+           "data": "device-drawn state and tokens with the workload's distributions"}
+    return out
 
 
 def copy_calibration(nbytes=1 << 30):
@@ -657,6 +825,13 @@ def main():
     S0 = prefill_state(wl, dims)
     log(f"[bench] prefill done ({time.time() - t0:.1f}s)")
 
+    if args.profile_decode:
+        ncold = cold_copies(wl)
+        cold = decode_rotating(wl, dims, S0, toks, copies=ncold, reps=2)
+        copy_calibration()
+        print(json.dumps({"profile_decode_us": round(cold * 1e3, 2), "rotating_batches": ncold}), flush=True)
+        return
+
     runner = Runner(wl, dims, S0, toks, use_graph=not args.no_graph)
     log("[bench] runner ready")
     secs, wall = time_steps(runner.step, args.steps, args.warmup)
@@ -680,9 +855,15 @@ def main():
     step_bytes = (sum(dec_bytes) * (wl.steps // W) + commit_bytes(wl, W) * wl.tiles * (wl.steps // W)
                   + quantize_bytes(wl) * wl.tiles)
     eff = step_bytes / (ms_step * 1e-3) / 1e9
-    log(f"[bench] decode {kt['decode_ms'] * 1e3:.1f} us/launch ({achieved:.0f} GB/s), "
+    log(f"[bench] decode {kt['decode_ms'] * 1e3:.1f} us/launch ({achieved:.0f} GB/s, codes cache-resident), "
         f"commit {kt['commit_ms'] * 1e3:.1f} us, quantize {kt['quantize_ms'] * 1e3:.1f} us")
     traffic = traffic_from_profile(wl)
+    # The roofline is taken where no batch's state can stay in the Infinity Cache
+    # between its steps: batches rotate launch by launch (cold_copies).
+    ncold = cold_copies(wl)
+    cold = decode_rotating(wl, dims, S0, toks, copies=ncold)
+    achieved_cold = dec_avg_bytes / (cold * 1e-3) / 1e9
+    log(f"[bench] decode with {ncold} rotating batches {cold * 1e3:.1f} us/launch ({achieved_cold:.0f} GB/s)")
 
     out = {
         "metric": "token-head decode steps/s + effective HBM GB/s (% of peak), speedup vs bf16 state",
@@ -699,20 +880,23 @@ def main():
                    "graph": not args.no_graph},
         "effective_gbps": round(eff, 1),
         "frac_of_hbm_peak": round(eff / PEAK_HBM_GBS, 4),
-        "roofline": {"kernel": "decode_step", "bound": "hbm", "achieved": round(achieved, 1),
-                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+        "roofline": {"kernel": "decode_step", "bound": "hbm", "achieved": round(achieved_cold, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved_cold / PEAK_HBM_GBS, 4),
                      "traffic": None if traffic is None else round(traffic),
-                     "bytes_per_launch": round(dec_avg_bytes), "avg_launch_us": round(kt["decode_ms"] * 1e3, 2)},
+                     "bytes_per_launch": round(dec_avg_bytes), "avg_launch_us": round(cold * 1e3, 2),
+                     "timing": f"{ncold} batches rotate launch by launch (positions 1..W), so every step reads "
+                               "its state from HBM",
+                     "cache_resident": {
+                         "avg_launch_us": round(kt["decode_ms"] * 1e3, 2), "achieved": round(achieved, 1),
+                         "frac": round(achieved / PEAK_HBM_GBS, 4),
+                         "note": "one batch, as in the headline step: its int8 codes (134 MB) can stay in the "
+                                 "256 MB Infinity Cache from one step to the next"}},
         "kernels_us": {"decode_avg": round(kt["decode_ms"] * 1e3, 2),
+                       "decode_avg_cold": round(cold * 1e3, 2),
                        "commit": round(kt["commit_ms"] * 1e3, 2),
                        "quantize": round(kt["quantize_ms"] * 1e3, 2)},
     }
 
-    two = decode_two_batches(wl, dims, S0, toks)
-    out["roofline"]["two_batch_decode"] = {
-        "avg_launch_us": round(two * 1e3, 2), "achieved": round(dec_avg_bytes / (two * 1e-3) / 1e9, 1),
-        "note": "two batches alternate, so no batch's codes stay in the Infinity Cache between its steps"}
-    log(f"[bench] decode with two alternating batches {two * 1e3:.1f} us/launch")
     if not args.no_variants:
         out["bulk_quantize"] = bulk_quantize()
         log(f"[bench] bulk quantize {out['bulk_quantize']}")
@@ -723,9 +907,17 @@ def main():
                                             "positions, then a commit masked to the group whose window ended); "
                                             "per decode step over one window cycle incl. commits")
         log(f"[bench] staggered windows {out['staggered_windows']}")
+        fs = fused_schedules(wl, dims, S0, toks)
+        dec_us = kt["decode_ms"] * 1e3
+        fs["commit_share_aligned"] = round(kt["commit_ms"] * 1e3 / (W * dec_us + kt["commit_ms"] * 1e3), 4)
+        fs["note"] = ("decode fused with the window-end commit (leapquant_decode_step_commit) against a "
+                      "decode launch plus a commit, aligned and staggered (G groups, one batch); per decode "
+                      "step over one window cycle incl. commits")
+        out["fused_commit"] = fs
+        log(f"[bench] fused commit {fs}")
     ceil = stream_read_ceiling()
     out["stream_read_ceiling"] = ceil
-    out["roofline"]["frac_of_stream_ceiling"] = round(achieved / ceil["gbps"], 4)
+    out["roofline"]["frac_of_stream_ceiling"] = round(achieved_cold / ceil["gbps"], 4)
     log(f"[bench] streaming-read ceiling {ceil}")
 
     if not args.no_variants and wl.name == "kda_kimi":
@@ -790,6 +982,18 @@ def main():
                         "commit_us": round(rk_["commit_ms"] * 1e3, 2)}
         log(f"[bench] rwkv7: {out['rwkv7']}")
         del r_toks
+
+    if not args.no_variants and wl.name == "kda_kimi":
+        # the other workload shapes: the GQA GDN layer with INT8 and E4M3 states,
+        # and the large-batch GDN stress case with its frequent commits (W = 32)
+        cl = {}
+        for cw in (synth.WORKLOADS["gdn_qwen3next"],
+                   synth.WORKLOADS["gdn_qwen3next"].with_(name="gdn_qwen3next_e4m3", code=synth.CODE_E4M3),
+                   synth.WORKLOADS["gdn_stress"]):
+            cl[cw.name] = config_line(cw, args)
+            log(f"[bench] {cw.name}: {cl[cw.name]}")
+            torch.cuda.empty_cache()
+        out["configs"] = cl
 
     if not args.no_baselines:
         q, k, v, a, b = toks

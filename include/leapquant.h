@@ -198,6 +198,24 @@ int32_t leapquant_decode_step_general(const lq_dims *dims, lq_state *st, const f
                                       void *stream);
 
 /*
+ * leapquant_decode_step_commit -- leapquant_decode_step, then, in the same
+ * launch, the window commit of every tile whose window this token filled
+ * (rec_len reached W).  Sec. 3.3 (the refit at the window end runs inside the
+ * decode kernel, beside the other tiles' state reads), Sec. 4.1
+ * "Implementation".  Arguments, layouts, validation and the device error rules
+ * are those of leapquant_decode_step.  Every tile is decoded exactly as there;
+ * a tile with rec_len == W - 1 before the call is then committed exactly as
+ * leapquant_window_commit commits a full window (all W records, the new one
+ * included) and leaves the call with rec_len = 0.  Requests at different window
+ * positions may share one launch; only the tiles that reach W commit.  A tile
+ * rejected by the decode (full or corrupt window) is not committed.
+ * dims->rule must be LQ_RULE_DELTA or LQ_RULE_ADD (LQ_EINVAL otherwise).
+ */
+int32_t leapquant_decode_step_commit(const lq_dims *dims, lq_state *st, const float *q,
+                                     const float *k, const float *v, const float *alpha,
+                                     const float *beta, float *o, void *stream);
+
+/*
  * leapquant_window_commit -- end the window of the selected tiles.  Sec. 3.3
  * (refit at the window end), Sec. 3.4 Eq. (smooth).
  *   mask  [B] int32 on the device, nonzero = commit every head of request b;

@@ -25,7 +25,8 @@ LQ_DEVERR_WINDOW_FULL = 1
 LQ_DEVERR_BAD_REC_LEN = 2
 
 EXPORTS = ("leapquant_state_bytes", "leapquant_quantize_state", "leapquant_decode_step",
-           "leapquant_decode_step_general", "leapquant_window_commit", "leapquant_baseline_step",
+           "leapquant_decode_step_general", "leapquant_decode_step_commit", "leapquant_window_commit",
+           "leapquant_baseline_step",
            "leapquant_baseline_step_general", "leapquant_dequantize_state",
            "leapquant_check_error", "leapquant_strerror", "leapquant_last_hip_error")
 
@@ -65,6 +66,7 @@ def _lib():
         L.leapquant_quantize_state.argtypes = [vp, vp, vp, vp]
         L.leapquant_decode_step.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.leapquant_decode_step_general.argtypes = [vp] * 10
+        L.leapquant_decode_step_commit.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.leapquant_window_commit.argtypes = [vp, vp, vp, vp]
         L.leapquant_baseline_step.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
         L.leapquant_baseline_step_general.argtypes = [vp, vp, i32] + [vp] * 8
@@ -235,6 +237,17 @@ def leapquant_decode_step(dims: lq_dims, st: State, q, k, v, alpha, beta, o, str
     _check(_lib().leapquant_decode_step(C.byref(dims), C.byref(s), _ptr(q), _ptr(k), _ptr(v),
                                         _ptr(alpha), _ptr(beta), _ptr(o), _stream(stream)),
            "leapquant_decode_step")
+
+
+def leapquant_decode_step_commit(dims: lq_dims, st: State, q, k, v, alpha, beta, o, stream=None):
+    """Decode step, then the commit of every tile whose window it filled, in one
+    launch."""
+    _check_state(dims, st)
+    _check_tokens(dims, q, k, v, alpha, beta, o)
+    s = st.struct()
+    _check(_lib().leapquant_decode_step_commit(C.byref(dims), C.byref(s), _ptr(q), _ptr(k), _ptr(v),
+                                               _ptr(alpha), _ptr(beta), _ptr(o), _stream(stream)),
+           "leapquant_decode_step_commit")
 
 
 def leapquant_decode_step_general(dims: lq_dims, st: State, q, k, b, v, alpha, beta, o,

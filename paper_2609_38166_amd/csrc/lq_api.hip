@@ -155,6 +155,18 @@ int32_t leapquant_decode_step(const lq_dims *d, lq_state *st, const float *q, co
     return hip_status(lq::launch_decode(*d, state_ptrs(st), t, (hipStream_t)stream));
 }
 
+int32_t leapquant_decode_step_commit(const lq_dims *d, lq_state *st, const float *q, const float *k,
+                                     const float *v, const float *alpha, const float *beta, float *o,
+                                     void *stream) {
+    int32_t e = check_dims(d);
+    if (e != LQ_OK) return e;
+    if ((e = check_state(d, st)) != LQ_OK) return e;
+    if (d->rule == LQ_RULE_GENERAL) return LQ_EINVAL;   // needs the read vectors
+    if ((e = check_tokens(d, q, k, v, alpha, beta, o)) != LQ_OK) return e;
+    lq::TokenPtrs t{q, k, v, alpha, beta, o, nullptr};
+    return hip_status(lq::launch_decode_commit(*d, state_ptrs(st), t, (hipStream_t)stream));
+}
+
 int32_t leapquant_decode_step_general(const lq_dims *d, lq_state *st, const float *q,
                                       const float *k, const float *b, const float *v,
                                       const float *alpha, const float *beta, float *o,

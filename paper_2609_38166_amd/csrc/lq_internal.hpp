@@ -33,6 +33,9 @@ struct TokenPtrs {
 
 hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &t, hipStream_t st);
 
+// decode step, then the window commit of every tile whose window it filled
+hipError_t launch_decode_commit(const lq_dims &d, const StatePtrs &s, const TokenPtrs &t, hipStream_t st);
+
 // mode: 0 = quantize given fp32 states, 1 = window commit, 2 = dequantize (read only)
 enum TileMode { TILE_QUANTIZE = 0, TILE_COMMIT = 1, TILE_DEQUANT = 2 };
 hipError_t launch_tile(const lq_dims &d, const StatePtrs &s, int mode, const float *S_in,

@@ -1,0 +1,161 @@
+"""The decode step fused with the window-end commit (leapquant_decode_step_commit).
+
+Two properties, through the C ABI:
+  - parity with the oracle: from the oracle's window-start representation, W
+    fused launches (the last one commits) give the oracle's outputs and the
+    oracle's next window-start representation, at the bars of the unfused path;
+  - equivalence with the unfused calls: on a staggered schedule (requests at
+    different window positions, so every launch holds decode-only and
+    decode-and-commit tiles) the fused launches give bit-identical outputs and
+    states to a decode launch followed by a commit of the requests whose window
+    just filled, at small and at full size.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_38166_amd import binding as B
+from paper_2609_38166_amd import synth
+from tests import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+
+W_ = synth.WORKLOADS
+PARITY = {
+    "gdn_tiny": W_["gdn_tiny"].with_(steps=48),
+    "kda_small": W_["kda_kimi"].with_(name="kda_small", batch=2, heads_v=4, heads_k=4, steps=128, prefill=256),
+    "gqa_e4m3_small": W_["gdn_qwen3next"].with_(name="gqa_e4m3_small", batch=2, heads_v=4, heads_k=2,
+                                                steps=64, prefill=256, code=synth.CODE_E4M3),
+    "kda_int4_small": W_["kda_kimi"].with_(name="kda_int4_small", batch=2, heads_v=4, heads_k=4, steps=64,
+                                           window=32, prefill=128, code=synth.CODE_INT4),
+    "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1, steps=32),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name", list(PARITY))
+def test_fused_window_parity(name):
+    wl = PARITY[name]
+    H.log(f"fused parity {name}")
+    cfg = H.ocfg(wl)
+    dims = H.gdims(wl)
+    S0 = H.oracle_prefill_state(wl)
+    streams, tok = H.decode_tokens(wl)
+    otok = synth.tile_major(wl, streams, tok)
+    ref = O.run_dense(cfg, S0, otok, snapshots=True, history=True)
+    dt = H.DeviceTokens(wl, tok)
+    st = B.State.empty(dims)
+    o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+    W = wl.window
+    tiles = np.arange(wl.tiles)
+    worst = {"o_rel": 0.0, "code_eq": 1.0, "code_maxdiff": 0, "deq_rel": 0.0, "comp_rel": 0.0,
+             "delta_rel": 0.0, "c_rel": 0.0}
+    for w in range(wl.steps // W):
+        H.upload_rep(st, tiles, *(ref[k_][:, w] for k_ in ("Z", "delta", "c", "Kt", "Ut")))
+        outs = []
+        for j in range(W):
+            B.leapquant_decode_step_commit(dims, st, *dt.step(w * W + j), o)
+            outs.append(o.view(wl.tiles, wl.dv).cpu().numpy())
+            n_exp = 0 if j == W - 1 else j + 1
+            assert np.all(st.rec_len.cpu().numpy() == n_exp), (w, j)
+        og = np.stack(outs, axis=1)
+        worst["o_rel"] = max(worst["o_rel"], H.rel_rows(og, ref["o"][:, w * W:(w + 1) * W]))
+        exp = {k_: ref[k_][:, w + 1] for k_ in ("Z", "delta", "c", "Kt", "Ut")}
+        cr = H.compare_rep(cfg, H.download_rep(st), exp, wl.code)
+        worst["code_eq"] = min(worst["code_eq"], cr["code_eq"])
+        for k_ in ("code_maxdiff", "deq_rel", "comp_rel", "delta_rel", "c_rel"):
+            worst[k_] = max(worst[k_], cr.get(k_, 0))
+    H.log(f"[{name} fused] {worst}")
+    assert B.leapquant_check_error(st) == 0
+    assert worst["o_rel"] <= 1e-3
+    assert worst["code_eq"] >= 0.999 and worst["code_maxdiff"] <= 1, worst
+    assert worst["deq_rel"] <= 1e-3 and worst["comp_rel"] <= 1e-3, worst
+    assert worst["delta_rel"] <= 1e-5 and worst["c_rel"] <= 1e-5, worst
+
+
+EQUIV = {
+    # (workload, groups): request b starts its window at offset (b % G) * W / G
+    "kda_small_g4": (W_["kda_kimi"].with_(name="kda_small", batch=8, heads_v=4, heads_k=4, window=16,
+                                          steps=40, prefill=64), 4),
+    "gdn_gqa_int6_g2": (W_["gdn_qwen3next"].with_(name="gdn_gqa_int6", batch=4, heads_v=4, heads_k=2,
+                                                  window=8, steps=20, prefill=64, code=synth.CODE_INT6), 2),
+    "gla_g3": (W_["kda_kimi"].with_(name="gla", batch=6, heads_v=2, heads_k=2, window=6, n_comp=2, steps=14,
+                                    prefill=64, rule=1), 3),
+    # the headline layer at full size, four request groups
+    "kda_kimi_full_g4": (W_["kda_kimi"].with_(steps=40), 4),
+}
+
+
+@pytest.mark.parametrize("name", list(EQUIV))
+def test_fused_equals_decode_then_commit(name):
+    wl, G = EQUIV[name]
+    H.log(f"fused vs unfused {name}")
+    dims = H.gdims(wl)
+    W, Bn, Hv = wl.window, wl.batch, wl.heads_v
+    g = torch.Generator(device="cuda")
+    g.manual_seed(wl.seed)
+    S = torch.randn((Bn, Hv, wl.dv, wl.dk), device="cuda", generator=g) * 0.1
+    fused = B.State.empty(dims)
+    B.leapquant_quantize_state(dims, S, fused)
+    del S
+    off = torch.as_tensor([(b % G) * W // G for b in range(Bn)], dtype=torch.int32, device="cuda")
+    fused.rec_len.copy_(off[:, None].expand(Bn, Hv))
+    # the open windows hold records of earlier tokens
+    fused.rec_k.copy_((torch.randn(fused.rec_k.shape, device="cuda", generator=g) * 0.05).half()
+                      .view(fused.rec_k.dtype))
+    fused.rec_u.copy_(torch.randn(fused.rec_u.shape, device="cuda", generator=g).half().view(fused.rec_u.dtype))
+    fused.rec_a.copy_((0.8 + 0.2 * torch.rand(fused.rec_a.shape, device="cuda", generator=g)).half()
+                      .view(fused.rec_a.dtype))
+    plain = B.State(dims, *[getattr(fused, f).clone() for f in B.FIELDS])
+    fst = synth.Streams(wl, synth.PHASE_DECODE)
+    dt = H.DeviceTokens(wl, fst.draw(wl.steps))
+    fst.close()
+    o_f = torch.empty((Bn, Hv, wl.dv), dtype=torch.float32, device="cuda")
+    o_p = torch.empty_like(o_f)
+    for t in range(wl.steps):
+        B.leapquant_decode_step_commit(dims, fused, *dt.step(t), o_f)
+        B.leapquant_decode_step(dims, plain, *dt.step(t), o_p)
+        full = (plain.rec_len[:, 0] == W).to(torch.int32)       # requests whose window just filled
+        B.leapquant_window_commit(dims, plain, full)
+        assert torch.equal(o_f, o_p), t
+        assert torch.equal(fused.rec_len, plain.rec_len), t
+    torch.cuda.synchronize()
+    for f in B.FIELDS:
+        if f == "err":
+            continue
+        if f in ("rec_k", "rec_u", "rec_a"):
+            # slots past a tile's rec_len are dead; the live ones must agree
+            n = plain.rec_len.view(-1).cpu().numpy()
+            x = getattr(fused, f).view(wl.tiles, W, -1).cpu().numpy()
+            y = getattr(plain, f).view(wl.tiles, W, -1).cpu().numpy()
+            for i in range(wl.tiles):
+                assert np.array_equal(x[i, :n[i]], y[i, :n[i]]), (f, i)
+        else:
+            assert torch.equal(getattr(fused, f), getattr(plain, f)), f
+    assert B.leapquant_check_error(fused) == 0 and B.leapquant_check_error(plain) == 0
+
+
+def test_fused_rejects_general_rule_and_keeps_device_errors():
+    wl = PARITY["gdn_tiny"].with_(window=2, steps=3)
+    dims = H.gdims(wl)
+    st = B.State.empty(dims)
+    _, tok = H.decode_tokens(wl)
+    dt = H.DeviceTokens(wl, tok)
+    o = torch.empty((wl.tiles, 128), dtype=torch.float32, device="cuda")
+    g = H.gdims(wl, rule=2)
+    with pytest.raises(B.LeapQuantError):
+        B.leapquant_decode_step_commit(g, st, *dt.step(0), o)
+    # a corrupt window length: the tile is untouched and not committed
+    st.rec_len.fill_(5)
+    B.leapquant_decode_step_commit(dims, st, *dt.step(0), o)
+    assert B.leapquant_check_error(st) == B.LQ_DEVERR_WINDOW_FULL
+    assert torch.all(st.rec_len == 5) and torch.isnan(o).all()
