@@ -68,7 +68,9 @@ typedef struct {
     int32_t n_comp;        /* r: Compensator Tokens */
     int32_t power_iters;   /* power-iteration sweeps per token */
     int32_t gate;          /* 0: scalar decay (GDN); 1: per-key-channel decay (KDA) */
-    int32_t code;          /* 0: INT8; 1: FP8 E4M3FN; 2: INT4; 3: INT6 codes */
+    int32_t code;          /* 0: INT8; 1: FP8 E4M3FN; 2: INT4; 3: INT6 codes; 4: BF16 state
+                            * (the window end rounds the state to BF16: unit scales,
+                            * no smoothing, no Compensator Tokens) */
     int32_t smooth;        /* 1: residual smoothing; 0: c = 1 */
     int32_t quantize;      /* 1: quantize at window ends; 0: keep the state exact */
     int32_t round_records; /* 1: FP16 records (alpha, write key, correction); 0: exact */
@@ -84,11 +86,14 @@ static real rec_round(const lqo_cfg *cfg, real x) { return cfg->round_records ? 
 
 /* Codes are held one per byte here (the packing of 4- and 6-bit codes is a
  * storage layout, not arithmetic): integer codes as two's-complement bytes,
- * E4M3 codes as their bit pattern. */
-static real code_value(const lqo_cfg *cfg, uint8_t z)
+ * E4M3 codes as their bit pattern; the BF16 state as two bytes per entry. */
+static size_t code_bytes(const lqo_cfg *cfg) { return cfg->code == 4 ? 2 : 1; }
+
+static real code_value(const lqo_cfg *cfg, const uint8_t *Z, size_t i)
 {
-    if (cfg->code == 1) return (real)lqo_e4m3_to_f32(z);
-    return (real)(int8_t)z;
+    if (cfg->code == 4) return (real)lqo_bf16_to_f32(((const uint16_t *)Z)[i]);
+    if (cfg->code == 1) return (real)lqo_e4m3_to_f32(Z[i]);
+    return (real)(int8_t)Z[i];
 }
 
 /* Largest code magnitude: 2^(b-1) - 1 for b-bit symmetric integers, 448 for E4M3. */
@@ -132,6 +137,14 @@ static void quantize_impl(const lqo_cfg *cfg, const double *S_in, uint8_t *Z, fl
                           float *c, double *Kt, double *Ut)
 {
     const int dk = cfg->dk, dv = cfg->dv, r = cfg->n_comp;
+    if (cfg->code == 4) {
+        /* BF16 state (the per-window BF16 variant of Sec. 3.2): each entry rounded
+         * to nearest even through fp32, unit scales, no tokens (r must be 0). */
+        for (int i = 0; i < dk * dv; ++i) ((uint16_t *)Z)[i] = lqo_f32_to_bf16((float)S_in[i]);
+        for (int k = 0; k < dk; ++k) c[k] = 1.0f;
+        for (int v = 0; v < dv; ++v) delta[v] = 1.0f;
+        return;
+    }
     real *M = (real *)malloc(sizeof(real) * (size_t)dk * dv);
     real *x = (real *)malloc(sizeof(real) * (size_t)dk);
     real *y = (real *)malloc(sizeof(real) * (size_t)dv);
@@ -246,7 +259,7 @@ void OQ(dequantize)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, co
     const int dk = cfg->dk, dv = cfg->dv;
     for (int k = 0; k < dk; ++k)
         for (int v = 0; v < dv; ++v) {
-            real s = (real)c[k] * (code_value(cfg, Z[k * dv + v]) * (real)delta[v]);
+            real s = (real)c[k] * (code_value(cfg, Z, (size_t)k * dv + v) * (real)delta[v]);
             for (int h = 0; h < cfg->n_comp; ++h)
                 s += (real)Kt[(size_t)h * dk + k] * (real)Ut[(size_t)h * dv + v];
             S[k * dv + v] = (double)s;
@@ -403,7 +416,7 @@ static void readout_impl(const lqo_cfg *cfg, const uint8_t *Z, const float *delt
     for (int v = 0; v < dv; ++v) {
         real s = 0;
         if (Z) {
-            for (int i = 0; i < dk; ++i) s += code_value(cfg, Z[i * dv + v]) * (real)c[i] * y[i];
+            for (int i = 0; i < dk; ++i) s += code_value(cfg, Z, (size_t)i * dv + v) * (real)c[i] * y[i];
             s *= (real)delta[v];
         } else {
             for (int i = 0; i < dk; ++i) s += (real)S0[i * dv + v] * y[i];
@@ -475,7 +488,7 @@ void OQ(reconstruct)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, c
         for (int v = 0; v < dv; ++v) {
             real base;
             if (Z) {
-                base = (real)c[i] * (code_value(cfg, Z[i * dv + v]) * (real)delta[v]);
+                base = (real)c[i] * (code_value(cfg, Z, (size_t)i * dv + v) * (real)delta[v]);
                 for (int h = 0; h < cfg->n_comp; ++h)
                     base += (real)Kt[(size_t)h * dk + i] * (real)Ut[(size_t)h * dv + v];
             } else {
@@ -495,7 +508,7 @@ void OQ(reconstruct)(const lqo_cfg *cfg, const uint8_t *Z, const float *delta, c
 /* ------------------------------------------------------------------------ */
 
 typedef struct {
-    uint8_t *Z;        /* [tiles][n_snap][dk][dv]  (may be NULL) */
+    uint8_t *Z;        /* [tiles][n_snap][dk][dv] x code bytes (may be NULL) */
     float *delta;      /* [tiles][n_snap][dv] */
     float *c;          /* [tiles][n_snap][dk] */
     double *Kt;        /* [tiles][n_snap][r][dk] */
@@ -543,7 +556,7 @@ static void store_snap(const lqo_cfg *cfg, const lqo_outputs *out, int tile, int
     if (!out->Z) return;
     const int dk = cfg->dk, dv = cfg->dv, r = cfg->n_comp;
     const size_t idx = (size_t)tile * n_snap_of(cfg, T) + s;
-    memcpy(out->Z + idx * dk * dv, Z, (size_t)dk * dv);
+    memcpy(out->Z + idx * dk * dv * code_bytes(cfg), Z, (size_t)dk * dv * code_bytes(cfg));
     memcpy(out->delta + idx * dv, delta, sizeof(float) * dv);
     memcpy(out->c + idx * dk, c, sizeof(float) * dk);
     if (r) {
@@ -567,7 +580,7 @@ int OQ(run_dense)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
         real *S = (real *)malloc(sizeof(real) * (size_t)dk * dv);
         double *Sd = (double *)malloc(sizeof(double) * (size_t)dk * dv);
         real *u = (real *)malloc(sizeof(real) * (size_t)dv);
-        uint8_t *Z = (uint8_t *)calloc((size_t)dk * dv, 1);
+        uint8_t *Z = (uint8_t *)calloc((size_t)dk * dv, code_bytes(cfg));
         float *delta = (float *)calloc((size_t)dv, sizeof(float));
         float *c = (float *)calloc((size_t)dk, sizeof(float));
         double *Kt = (double *)calloc((size_t)(r ? r : 1) * dk, sizeof(double));
@@ -630,7 +643,7 @@ int OQ(run_readout)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
 #pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads > 0 ? n_threads : 1)
     for (int t = 0; t < tiles; ++t) {
         double *Sd = (double *)malloc(sizeof(double) * (size_t)dk * dv);
-        uint8_t *Z = (uint8_t *)calloc((size_t)dk * dv, 1);
+        uint8_t *Z = (uint8_t *)calloc((size_t)dk * dv, code_bytes(cfg));
         float *delta = (float *)calloc((size_t)dv, sizeof(float));
         float *c = (float *)calloc((size_t)dk, sizeof(float));
         double *Kt = (double *)calloc((size_t)(r ? r : 1) * dk, sizeof(double));
@@ -710,7 +723,10 @@ int OQ(run_baseline)(const lqo_cfg *cfg, int tiles, int T, const double *S_init,
  * Drift of the per-window quantized trajectory (O3) from the unquantized fp32
  * trajectory (O5, fp32 state) driven by the same tokens (App. B.1): every
  * `every` tokens, ||S_window - S_fp32||_F / ||S_fp32||_F and the relative L2
- * error of that token's output.  drift and odrift are [tiles][T/every].
+ * error of that token's output.  drift and odrift are [tiles][T/every].  With
+ * cfg->quantize == 0 the window path starts from the fp32 state and is never
+ * quantized (then, in the fp32 build with exact records, both trajectories take
+ * the same operations).
  */
 int OQ(run_drift)(const lqo_cfg *cfg, int tiles, int T, int every, const double *S_init,
                   const lqo_inputs *in, double *drift, double *odrift, int n_threads)
@@ -725,7 +741,7 @@ int OQ(run_drift)(const lqo_cfg *cfg, int tiles, int T, int every, const double 
         real *u = (real *)malloc(sizeof(real) * (size_t)dv);
         double *o1 = (double *)malloc(sizeof(double) * (size_t)dv);
         double *o2 = (double *)malloc(sizeof(double) * (size_t)dv);
-        uint8_t *Z = (uint8_t *)calloc((size_t)dk * dv, 1);
+        uint8_t *Z = (uint8_t *)calloc((size_t)dk * dv, code_bytes(cfg));
         float *delta = (float *)calloc((size_t)dv, sizeof(float));
         float *c = (float *)calloc((size_t)dk, sizeof(float));
         double *Kt = (double *)calloc((size_t)(r ? r : 1) * dk, sizeof(double));
@@ -735,9 +751,13 @@ int OQ(run_drift)(const lqo_cfg *cfg, int tiles, int T, int every, const double 
         double *ru = (double *)calloc((size_t)dv, sizeof(double));
         const double *S0 = S_init + (size_t)t * dk * dv;
         for (int i = 0; i < dk * dv; ++i) F[i] = (real)(float)S0[i];
-        quantize_impl(cfg, S0, Z, delta, c, Kt, Ut);
-        OQ(dequantize)(cfg, Z, delta, c, Kt, Ut, Sd);
-        for (int i = 0; i < dk * dv; ++i) S[i] = (real)Sd[i];
+        if (cfg->quantize) {
+            quantize_impl(cfg, S0, Z, delta, c, Kt, Ut);
+            OQ(dequantize)(cfg, Z, delta, c, Kt, Ut, Sd);
+            for (int i = 0; i < dk * dv; ++i) S[i] = (real)Sd[i];
+        } else {
+            for (int i = 0; i < dk * dv; ++i) S[i] = (real)(float)S0[i];
+        }
         int n = 0;
         for (int s = 0; s < T; ++s) {
             const size_t ts = (size_t)t * T + s;
@@ -746,10 +766,12 @@ int OQ(run_drift)(const lqo_cfg *cfg, int tiles, int T, int every, const double 
             recurrent_step_impl(cfg, F, in->q + ts * dk, in->k + ts * dk, read_vec(in, ts, dk),
                                 in->v + ts * dv, in->alpha + ts * g, in->beta[ts], o2, LQO_STATE_F32, u);
             if (++n == W) {
-                for (int i = 0; i < dk * dv; ++i) Sd[i] = (double)S[i];
-                quantize_impl(cfg, Sd, Z, delta, c, Kt, Ut);
-                OQ(dequantize)(cfg, Z, delta, c, Kt, Ut, Sd);
-                for (int i = 0; i < dk * dv; ++i) S[i] = (real)Sd[i];
+                if (cfg->quantize) {
+                    for (int i = 0; i < dk * dv; ++i) Sd[i] = (double)S[i];
+                    quantize_impl(cfg, Sd, Z, delta, c, Kt, Ut);
+                    OQ(dequantize)(cfg, Z, delta, c, Kt, Ut, Sd);
+                    for (int i = 0; i < dk * dv; ++i) S[i] = (real)Sd[i];
+                }
                 n = 0;
             }
             if ((s + 1) % every == 0 && (s + 1) / every <= nd) {

@@ -51,13 +51,18 @@ class _Outputs(C.Structure):
 
 GATE_SCALAR, GATE_DIAG = 0, 1
 RULE_DELTA, RULE_ADD, RULE_GENERAL = 0, 1, 2   # b_t = D_t k_t (delta rule), b_t = 0, b_t given
-CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6 = 0, 1, 2, 3
+CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6, CODE_BF16 = 0, 1, 2, 3, 4
 STATE_EXACT, STATE_F32, STATE_BF16 = 0, 1, 2
 
 
 def make_cfg(dk=128, dv=128, window=16, n_comp=4, power_iters=4, gate=GATE_SCALAR,
              code=CODE_INT8, smooth=1, quantize=1, round_records=1, rule=RULE_DELTA) -> Cfg:
     return Cfg(dk, dv, window, n_comp, power_iters, gate, code, smooth, quantize, round_records, rule)
+
+
+def code_dtype(cfg: Cfg):
+    """Storage of one code: a byte, or the two bytes of a BF16 state entry."""
+    return np.uint16 if cfg.code == CODE_BF16 else np.uint8
 
 
 def _p(a):
@@ -131,7 +136,7 @@ def e4m3_to_f32(b) -> np.ndarray:
 @dataclass
 class Rep:
     """Quantized window-start representation of one tile."""
-    Z: np.ndarray       # uint8 [dk][dv] code bytes
+    Z: np.ndarray       # uint8 [dk][dv] code bytes (uint16 BF16 bits for the BF16 state)
     delta: np.ndarray   # float32 [dv]
     c: np.ndarray       # float32 [dk]
     Kt: np.ndarray      # float64 [r][dk] (FP16 values)
@@ -141,7 +146,7 @@ class Rep:
 def quantize(cfg: Cfg, S, prec=64) -> Rep:
     S = np.ascontiguousarray(S, dtype=np.float64)
     r = max(cfg.n_comp, 1)
-    rep = Rep(np.zeros((cfg.dk, cfg.dv), np.uint8), np.zeros(cfg.dv, np.float32),
+    rep = Rep(np.zeros((cfg.dk, cfg.dv), code_dtype(cfg)), np.zeros(cfg.dv, np.float32),
               np.zeros(cfg.dk, np.float32), np.zeros((r, cfg.dk)), np.zeros((r, cfg.dv)))
     _fn("quantize", prec)(C.byref(cfg), _p(S), _p(rep.Z), _p(rep.delta), _p(rep.c),
                           _p(rep.Kt), _p(rep.Ut))
@@ -272,7 +277,7 @@ def _run_window(name, cfg: Cfg, S_init, tok: dict, snapshots=True, threads=None,
            "rec_a": np.zeros((tiles, W, g)), "rec_k": np.zeros((tiles, W, cfg.dk)),
            "rec_u": np.zeros((tiles, W, cfg.dv)), "rec_len": np.zeros(tiles, np.int32)}
     if snapshots:
-        res.update({"Z": np.zeros((tiles, ns, cfg.dk, cfg.dv), np.uint8),
+        res.update({"Z": np.zeros((tiles, ns, cfg.dk, cfg.dv), code_dtype(cfg)),
                     "delta": np.zeros((tiles, ns, cfg.dv), np.float32),
                     "c": np.zeros((tiles, ns, cfg.dk), np.float32),
                     "Kt": np.zeros((tiles, ns, r, cfg.dk)), "Ut": np.zeros((tiles, ns, r, cfg.dv))})

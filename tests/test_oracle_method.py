@@ -609,3 +609,132 @@ def test_per_window_drifts_less_than_per_step(O):
     d_step, _ = O.run_drift(O.make_cfg(dk=dk, dv=dv, window=1, n_comp=0, smooth=0), S0, tok, 64)
     d_win, _ = O.run_drift(O.make_cfg(dk=dk, dv=dv, window=16, n_comp=4), S0, tok, 64)
     assert np.mean(d_win) < 0.5 * np.mean(d_step)
+
+
+# --------------------------------------------------------------------------- BF16 state (code 4)
+
+def _bf16(x):
+    """fp32 -> bf16 (round to nearest even) -> float64, by torch (not the oracle)."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16).to(
+        torch.float64).numpy()
+
+
+def test_bf16_state_quantizer_is_bf16_rounding(O):
+    """Code 4 keeps the state itself in BF16: the window-end quantizer is the
+    round-to-nearest-even BF16 rounding of the fp32 value, with unit scales and no
+    smoothing.  Checked against torch's conversion, ties and subnormals included."""
+    import torch
+    rng = np.random.default_rng(120)
+    dk = dv = 32
+    S = rng.standard_normal((dk, dv)) * np.exp(rng.uniform(-30, 30, (dk, dv)))
+    b = np.float32(rng.standard_normal(64)).view(np.uint32)
+    ties = ((b & 0xFFFF0000) | 0x8000).view(np.float32)          # exactly half-way between two bf16
+    S.flat[:64] = ties
+    S.flat[64:72] = np.float32([1e-39, -3e-40, 0.0, -0.0, 1e-45, 3.4e38, -1.17e-38, 7e-39])
+    cfg = O.make_cfg(dk=dk, dv=dv, n_comp=0, code=O.CODE_BF16)
+    rep = O.quantize(cfg, S)
+    ref = torch.from_numpy(S.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert rep.Z.dtype == np.uint16 and np.array_equal(rep.Z, ref)
+    assert np.all(rep.delta == 1.0) and np.all(rep.c == 1.0)
+    assert np.array_equal(O.dequantize(cfg, rep), _bf16(S.astype(np.float32)))
+
+
+@pytest.mark.parametrize("gate", [0, 1])
+@pytest.mark.parametrize("W", [1, 5])
+def test_bf16_per_window_is_recurrence_rounded_at_window_ends(O, gate, W):
+    """The per-window BF16 state (Sec. 3.2, the BF16 rows of the ablation): the
+    unquantized recurrence, written out with the explicit delta-rule formulas,
+    with the state rounded to BF16 through fp32 at the start and after every W
+    tokens (exact records, so only the window-end rounding differs from the
+    recurrence)."""
+    rng = np.random.default_rng(121 + gate + W)
+    dk = dv = 32
+    T = 3 * W + 2
+    S0 = rng.standard_normal((1, dk, dv))
+    tok = _tokens(rng, 1, T, dk, dv, gate)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=W, n_comp=0, gate=gate, code=O.CODE_BF16, smooth=0,
+                     round_records=0)
+    res = O.run_dense(cfg, S0, tok, snapshots=True)
+    S = _bf16(S0[0].astype(np.float32))
+    assert np.array_equal(O.dequantize(cfg, O.Rep(res["Z"][0, 0], res["delta"][0, 0], res["c"][0, 0],
+                                                  np.zeros((0, dk)), np.zeros((0, dv)))), S)
+    for t in range(T):
+        q, k, v = (tok[n][0, t].astype(np.float64) for n in ("q", "k", "v"))
+        a = tok["alpha"][0, t].astype(np.float64)
+        b = np.float64(tok["beta"][0, t])
+        A = (a[:, None] if gate else a[0]) * S
+        S = A + np.outer(b * k, v - A.T @ k)
+        assert rel(res["o"][0, t], S.T @ q) < 1e-12
+        if (t + 1) % W == 0:
+            S = _bf16(S.astype(np.float32))
+            bits = (S.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+            assert np.array_equal(res["Z"][0, (t + 1) // W], bits)
+
+
+def test_bf16_per_step_is_the_bf16_baseline(O):
+    """W = 1 with exact records: the per-window BF16 state after every token is
+    the per-step BF16 baseline's state (the state rounded to BF16 after each
+    update), bit for bit."""
+    rng = np.random.default_rng(125)
+    dk = dv = 32
+    S0 = _bf16(rng.standard_normal((2, dk, dv)).astype(np.float32))
+    tok = _tokens(rng, 2, 17, dk, dv, 1)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=1, n_comp=0, gate=1, code=O.CODE_BF16, round_records=0)
+    res = O.run_dense(cfg, S0, tok, snapshots=False)
+    _, S_b = O.run_baseline(cfg, S0, tok, mode=O.STATE_BF16)
+    assert np.array_equal(res["S_final"], S_b)
+
+
+@pytest.mark.parametrize("gate", [0, 1])
+def test_bf16_readout_form_equals_dense_form(O, gate):
+    rng = np.random.default_rng(126 + gate)
+    dk = dv = 64
+    S0 = _state(rng, dk, dv)[None].repeat(2, 0)
+    tok = _tokens(rng, 2, 40, dk, dv, gate)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=16, n_comp=0, gate=gate, code=O.CODE_BF16, smooth=0)
+    d, b = O.run_dense(cfg, S0, tok), O.run_readout(cfg, S0, tok)
+    assert rel(b["o"], d["o"]) < 1e-10
+    assert np.mean(b["Z"] == d["Z"]) > 0.9999
+    assert rel(b["S_final"], d["S_final"]) < 1e-10
+
+
+# --------------------------------------------------------------------------- drift (App. B.1)
+
+def test_drift_is_zero_without_quantization(O):
+    """Quantization off and exact records: in the fp32 build the window path and
+    the fp32 recurrence take the same operations, so the drift is exactly 0."""
+    rng = np.random.default_rng(130)
+    dk = dv = 32
+    S0 = rng.standard_normal((3, dk, dv)).astype(np.float32).astype(np.float64)
+    tok = _tokens(rng, 3, 64, dk, dv, 1)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=16, n_comp=4, gate=1, quantize=0, round_records=0)
+    drift, odrift = O.run_drift(cfg, S0, tok, 8, prec=32)
+    assert drift.shape == (3, 8) and not drift.any() and not odrift.any()
+
+
+@pytest.mark.parametrize("gate", [0, 1])
+def test_drift_bookkeeping_against_explicit_fp32_recurrence(O, gate):
+    """run_drift's sampled drift equals ||S_window(t) - F(t)|| / ||F(t)|| with the
+    window state taken from the dense trajectory after t tokens and F the fp32
+    recurrence written out here (fp64 update, rounded to fp32 after every token),
+    at window ends and inside windows; and likewise for the outputs."""
+    rng = np.random.default_rng(131 + gate)
+    dk = dv = 16
+    T, W, every = 12, 3, 2
+    S0 = rng.standard_normal((1, dk, dv)).astype(np.float32).astype(np.float64)
+    tok = _tokens(rng, 1, T, dk, dv, gate)
+    cfg = O.make_cfg(dk=dk, dv=dv, window=W, n_comp=1, gate=gate)
+    drift, odrift = O.run_drift(cfg, S0, tok, every)
+    F = S0[0].copy()
+    for t in range(T):
+        q, k, v = (tok[n][0, t].astype(np.float64) for n in ("q", "k", "v"))
+        a = tok["alpha"][0, t].astype(np.float64)
+        A = (a[:, None] if gate else a[0]) * F
+        F = (A + np.outer(np.float64(tok["beta"][0, t]) * k, v - A.T @ k)).astype(np.float32).astype(np.float64)
+        if (t + 1) % every == 0:
+            sub = {n_: x[:, :t + 1] for n_, x in tok.items()}
+            win = O.run_dense(cfg, S0, sub, snapshots=False)
+            Sw, ow = win["S_final"][0], win["o"][0, t]
+            assert abs(drift[0, (t + 1) // every - 1] - rel(Sw, F)) <= 1e-12 * rel(Sw, F)
+            assert abs(odrift[0, (t + 1) // every - 1] - rel(ow, F.T @ q)) <= 1e-12 * rel(ow, F.T @ q)
