@@ -63,7 +63,12 @@ def rec_bytes(wl):
     return 2 * (wl.dk + wl.dv) + 2 * wl.g          # FP16 key, correction, decay
 
 
-CODE_BITS = {0: 8, 1: 8, 2: 4, 3: 6}
+CODE_BITS = {0: 8, 1: 8, 2: 4, 3: 6, 4: 16}
+
+
+def scale_bytes(wl):
+    """Row scales and smoothing; the BF16 state (code 4) has none."""
+    return 0 if wl.code == 4 else 4 * (wl.dk + wl.dv)
 
 
 def code_bytes(wl):
@@ -73,12 +78,12 @@ def code_bytes(wl):
 def decode_bytes(wl, i):
     """Algorithmic bytes of one tile's decode at window position i (1-based)."""
     inputs = 4 * (2 * wl.dk) * wl.heads_k / wl.heads_v + 4 * wl.dv + 4 * wl.g + 4
-    return (code_bytes(wl) + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+    return (code_bytes(wl) + scale_bytes(wl) + 2 * wl.n_comp * (wl.dk + wl.dv)
             + (i - 1) * rec_bytes(wl) + rec_bytes(wl) + inputs + 4 * wl.dv + 8)
 
 
 def rep_bytes(wl):
-    return code_bytes(wl) + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+    return code_bytes(wl) + scale_bytes(wl) + 2 * wl.n_comp * (wl.dk + wl.dv)
 
 
 def commit_bytes(wl, p):
@@ -403,7 +408,7 @@ def decode_rotating(wl, dims, S0, toks, copies=2, reps=3):
 def cold_copies(wl):
     """Batches to rotate so that the others' state (codes, scales, compensators
     and the window's records) exceeds 512 MB, twice the Infinity Cache."""
-    per = wl.tiles * (code_bytes(wl) + 4 * (wl.dk + wl.dv) + 2 * wl.n_comp * (wl.dk + wl.dv)
+    per = wl.tiles * (code_bytes(wl) + scale_bytes(wl) + 2 * wl.n_comp * (wl.dk + wl.dv)
                       + wl.window * rec_bytes(wl))
     return max(2, 1 + int(np.ceil(512e6 / per)))
 
@@ -745,7 +750,8 @@ def cpu_baseline(wl, n_tiles):
 
 # ----------------------------------------------------------------------------- sweep
 
-SWEEP = (  # label, W, r, smooth  (INT8 codes)
+SWEEP = (  # label, W, r, smooth, code (0: INT8, 4: BF16 state)
+    ("bf16 per-window", 16, 0, 0, 4),
     ("int8 per-step", 1, 0, 0),
     ("int8 per-window", 16, 0, 0),
     ("+ compensator tokens", 16, 4, 0),
@@ -786,13 +792,15 @@ def sweep(args):
         print(json.dumps({"sweep": f"{name} per-step", "us_per_step": round(res[name], 2),
                           "speedup_vs_fp32": round(res["fp32"] / res[name], 3)}), flush=True)
         del S
-    for label, W, r, smooth in SWEEP:
-        wl = base.with_(window=W, n_comp=r, smooth=smooth)
+    for row in SWEEP:
+        label, W, r, smooth = row[:4]
+        code = row[4] if len(row) > 4 else base.code
+        wl = base.with_(window=W, n_comp=r, smooth=smooth, code=code)
         dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=W, n_comp=r,
                             power_iters=wl.power_iters, gate=wl.gate, code=wl.code, smooth=smooth)
         kt = per_launch_times(wl, dims, S0, toks)
         step = kt["decode_ms"] * 1e3 + kt["commit_ms"] * 1e3 / W
-        print(json.dumps({"sweep": label, "window": W, "n_comp": r, "smooth": smooth,
+        print(json.dumps({"sweep": label, "window": W, "n_comp": r, "smooth": smooth, "code": code,
                           "decode_us": round(kt["decode_ms"] * 1e3, 2),
                           "commit_us": round(kt["commit_ms"] * 1e3, 2),
                           "us_per_step": round(step, 2),
@@ -944,10 +952,10 @@ def main():
 
         # the same layer with the paper's lower-bit residual codes (same inputs)
         var = {}
-        for vname in ("kda_kimi_int6", "kda_kimi_int4"):
+        for vname in ("kda_kimi_int6", "kda_kimi_int4", "kda_kimi_bf16w"):
             vw = synth.WORKLOADS[vname]
             vd = B_.make_dims(vw.batch, vw.heads_v, vw.heads_k, window=vw.window, n_comp=vw.n_comp,
-                              power_iters=vw.power_iters, gate=vw.gate, code=vw.code)
+                              power_iters=vw.power_iters, gate=vw.gate, code=vw.code, smooth=vw.smooth)
             vk = per_launch_times(vw, vd, S0, toks)
             vstep = (vk["decode_ms"] * vw.steps + vk["commit_ms"] * (vw.steps // vw.window)
                      + vk["quantize_ms"])

@@ -64,6 +64,9 @@ extern "C" {
 #define LQ_CODE_E4M3   1     /* OCP FP8 E4M3FN codes, dequant = e4m3(code) * delta_v  */
 #define LQ_CODE_INT4   2     /* symmetric 4-bit, |code| <= 7, two codes per byte      */
 #define LQ_CODE_INT6   3     /* symmetric 6-bit, |code| <= 31, four codes per 3 bytes  */
+#define LQ_CODE_BF16   4     /* the state itself in BF16 (per-window BF16, Sec. 3.2):
+                              * rounded to nearest even at each window end; unit
+                              * scales, no smoothing, n_comp must be 0            */
 #define LQ_RULE_DELTA  0     /* delta rule: b_t = D_t k_t (DeltaNet, GDN, KDA)        */
 #define LQ_RULE_ADD    1     /* b_t = 0: u_t = v_t (linear attention, RetNet, Mamba2,
                               * GLA / RWKV6 / HGRN2 with the matching gate)           */
@@ -94,7 +97,8 @@ typedef struct {
     int32_t n_comp;      /* r in [0, 16]: Compensator Tokens per tile                */
     int32_t power_iters; /* power-iteration sweeps per token, >= 1 when r > 0        */
     int32_t gate;        /* LQ_GATE_SCALAR or LQ_GATE_DIAG                            */
-    int32_t code;        /* LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4 or LQ_CODE_INT6  */
+    int32_t code;        /* LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4, LQ_CODE_INT6 or
+                          * LQ_CODE_BF16                                          */
     int32_t smooth;      /* 1: residual smoothing (Sec. 3.4); 0: c = 1               */
     int32_t rule;        /* LQ_RULE_DELTA, LQ_RULE_ADD or LQ_RULE_GENERAL: the read
                           * vector b_t of the general recurrence (App. A table).
@@ -106,13 +110,16 @@ typedef struct {
 /* The quantized state of all tiles (device pointers, caller-owned).
  * Sizes per tile; g = 1 for the scalar gate, g = d_k for the diagonal gate. */
 typedef struct {
-    void     *codes;   /* [d_v][d_k*b/8] bytes, b = 8, 8, 4, 6 bits per code:
+    void     *codes;   /* [d_v][d_k*b/8] bytes, b = 8, 8, 4, 6, 16 bits per code:
                         *   INT8: one two's-complement byte per key channel;
                         *   E4M3: one E4M3FN byte per key channel;
                         *   INT4: byte i holds channel 2i (low nibble) and 2i+1
                         *         (high nibble), two's complement;
                         *   INT6: bytes 3i..3i+2, read little-endian as 24 bits,
-                        *         hold channels 4i..4i+3 at bits 6q..6q+5       */
+                        *         hold channels 4i..4i+3 at bits 6q..6q+5;
+                        *   BF16: the state value of each key channel in BF16
+                        *         (scale and smooth are then written as 1 by
+                        *         quantize and commit and never read)       */
     float    *scale;   /* [d_v]  delta_v = max_k |R^C_kv| / 127 (INT8) or / 448    */
     float    *smooth;  /* [d_k]  c_k, the residual smoothing scale                 */
     uint16_t *comp_k;  /* [r][d_k] fp16 key vectors k~_h of the Compensator Tokens */

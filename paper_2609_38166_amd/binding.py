@@ -17,8 +17,8 @@ LIB_PATH = os.path.join(_PKG, "libleapquant.so")
 
 LQ_OK, LQ_EINVAL, LQ_EALIGN, LQ_EUNSUPPORTED, LQ_EHIP, LQ_EDEVICE = 0, -1, -2, -3, -4, -5
 LQ_GATE_SCALAR, LQ_GATE_DIAG = 0, 1
-LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4, LQ_CODE_INT6 = 0, 1, 2, 3
-CODE_BITS = {LQ_CODE_INT8: 8, LQ_CODE_E4M3: 8, LQ_CODE_INT4: 4, LQ_CODE_INT6: 6}
+LQ_CODE_INT8, LQ_CODE_E4M3, LQ_CODE_INT4, LQ_CODE_INT6, LQ_CODE_BF16 = 0, 1, 2, 3, 4
+CODE_BITS = {LQ_CODE_INT8: 8, LQ_CODE_E4M3: 8, LQ_CODE_INT4: 4, LQ_CODE_INT6: 6, LQ_CODE_BF16: 16}
 LQ_STATE_F32, LQ_STATE_BF16 = 0, 1
 LQ_RULE_DELTA, LQ_RULE_ADD, LQ_RULE_GENERAL = 0, 1, 2
 LQ_DEVERR_WINDOW_FULL = 1

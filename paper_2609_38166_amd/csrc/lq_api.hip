@@ -35,13 +35,14 @@ int32_t check_dims(const lq_dims *d) {
     if (d->heads_v % d->heads_k != 0) return LQ_EINVAL;
     if (d->gate != LQ_GATE_SCALAR && d->gate != LQ_GATE_DIAG) return LQ_EINVAL;
     if (d->code != LQ_CODE_INT8 && d->code != LQ_CODE_E4M3 && d->code != LQ_CODE_INT4 &&
-        d->code != LQ_CODE_INT6)
+        d->code != LQ_CODE_INT6 && d->code != LQ_CODE_BF16)
         return LQ_EINVAL;
     if (d->smooth != 0 && d->smooth != 1) return LQ_EINVAL;
     if (d->rule != LQ_RULE_DELTA && d->rule != LQ_RULE_ADD && d->rule != LQ_RULE_GENERAL)
         return LQ_EINVAL;
     if (d->d_k != 128 || d->d_v != 128) return LQ_EUNSUPPORTED;
     if (d->n_comp > LQ_MAX_COMP) return LQ_EUNSUPPORTED;
+    if (d->code == LQ_CODE_BF16 && d->n_comp != 0) return LQ_EUNSUPPORTED;   // no tokens on a BF16 state
     if (d->n_comp > 0 && (d->power_iters < 1 || d->power_iters > LQ_MAX_POWER_ITERS))
         return LQ_EUNSUPPORTED;
     const int wmax = d->gate == LQ_GATE_DIAG ? LQ_MAX_WINDOW_KDA : LQ_MAX_WINDOW_GDN;
@@ -120,7 +121,7 @@ int32_t leapquant_state_bytes(const lq_dims *d, size_t out[10]) {
     if (!out) return LQ_EINVAL;
     const size_t t = (size_t)d->batch * d->heads_v, dk = d->d_k, dv = d->d_v;
     const size_t r = d->n_comp, W = d->window, g = d->gate == LQ_GATE_DIAG ? dk : 1;
-    const size_t bits = d->code == LQ_CODE_INT4 ? 4 : d->code == LQ_CODE_INT6 ? 6 : 8;
+    const size_t bits = d->code == LQ_CODE_INT4 ? 4 : d->code == LQ_CODE_INT6 ? 6 : d->code == LQ_CODE_BF16 ? 16 : 8;
     out[0] = t * dv * dk * bits / 8;   // codes
     out[1] = t * dv * 4;         // scale
     out[2] = t * dk * 4;         // smooth

@@ -5,8 +5,12 @@ namespace lq {
 
 namespace {
 
+// Four workgroups per CU; the BF16 state's 32 KiB of codes per tile in LDS
+// leave room for two.
+template <int CODE> struct DecodeOcc { static constexpr int value = IsBF16<CODE>::value ? 2 : 4; };
+
 template <int GATE, int CODE, int RULE>
-__global__ __launch_bounds__(NT, 4) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(NT, DecodeOcc<CODE>::value) void decode_kernel(DecodeArgs a) {
     __shared__ DecodeShared<CODE> sh;
     decode_body<GATE, CODE, RULE>(a, sh, blockIdx.x);
 }
@@ -31,6 +35,7 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
             case LQ_CODE_E4M3: return launch<1, 1>(a, d.rule, st);
             case LQ_CODE_INT4: return launch<1, 2>(a, d.rule, st);
             case LQ_CODE_INT6: return launch<1, 3>(a, d.rule, st);
+            case LQ_CODE_BF16: return launch<1, 4>(a, d.rule, st);
             default: return launch<1, 0>(a, d.rule, st);
         }
     }
@@ -38,6 +43,7 @@ hipError_t launch_decode(const lq_dims &d, const StatePtrs &s, const TokenPtrs &
         case LQ_CODE_E4M3: return launch<0, 1>(a, d.rule, st);
         case LQ_CODE_INT4: return launch<0, 2>(a, d.rule, st);
         case LQ_CODE_INT6: return launch<0, 3>(a, d.rule, st);
+        case LQ_CODE_BF16: return launch<0, 4>(a, d.rule, st);
         default: return launch<0, 0>(a, d.rule, st);
     }
 }

@@ -258,7 +258,7 @@ __device__ __forceinline__ void base_vectors(DecodeShared<CODE> &sh, double G, f
     sh.yk[t] = yk;
     sh.yq[t] = (float)yq;
     const double wk = (double)cs * yk, wq = (double)cs * yq;
-    if (CODE == 1) {
+    if (CODE == 1 || CODE == 4) {
         double *wkv = (double *)sh.rv;
         float *wqv = (float *)(sh.rv + D * 8);
         if (KS) wkv[ch] = wk;
@@ -324,6 +324,39 @@ __device__ __forceinline__ void code_product_e4m3(const DecodeShared<CODE> &sh, 
                 sk = fma((double)f1, wa.y, sk);
                 sk = fma((double)f2, wb.x, sk);
                 sk = fma((double)f3, wb.y, sk);
+            }
+        }
+    }
+    zk = sk;
+    zq = sq;
+}
+
+// BF16-state code product of one half row: thread (v, h) sums over channels
+// 64h .. 64h+63 of row v (eight 16-byte chunks of eight values), k side in
+// fp64, q side in fp32.
+template <int CODE, bool KS>
+__device__ __forceinline__ void code_product_bf16(const DecodeShared<CODE> &sh, int v, int h, double &zk,
+                                                  float &zq) {
+    const double *wkv = (const double *)sh.rv;
+    const float *wqv = (const float *)(sh.rv + D * 8);
+    double sk = 0.0;
+    float sq = 0.0f;
+#pragma unroll 2
+    for (int m = 0; m < 8; ++m) {
+        const int c = 8 * h + m;
+        const uint4 z = lds_chunk<CODE>(sh.codes, v, c);
+        const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const int c0 = 8 * c + 2 * p;          // channels c0, c0 + 1
+            const float f0 = __uint_as_float(zw[p] << 16), f1 = __uint_as_float(zw[p] & 0xFFFF0000u);
+            const float2 wq = *(const float2 *)&wqv[c0];
+            sq = fmaf(f0, wq.x, sq);
+            sq = fmaf(f1, wq.y, sq);
+            if (KS) {
+                const double2 wk = *(const double2 *)&wkv[c0];
+                sk = fma((double)f0, wk.x, sk);
+                sk = fma((double)f1, wk.y, sk);
             }
         }
     }
@@ -456,7 +489,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
     if (tid < D) {
         kx = ((gf *)pk)[kvec + ch];
         qx = ((gf *)pq)[kvec + ch];
-        cs = ((gf *)pc)[tvec + ch];
+        cs = IsBF16<CODE>::value ? 1.0f : ((gf *)pc)[tvec + ch];
         if (GATE) al = ((gf *)pa)[tvec + ch];
         vx = ((gf *)pv)[tvec + ch];
         if (RULE == LQ_RULE_GENERAL) bx = ((gf *)pb)[tvec + ch];
@@ -473,7 +506,8 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             dma16(zt + v * SEGS + ((c - zrot<CODE>(v) + SEGS) % SEGS), lds_addr(&sh.codes[NT * m + 64 * w]));
         }
     }
-    if (tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(sh.dlt));   // per-row scales, wave 0
+    // per-row scales, wave 0 (the BF16 state has unit scales and does not read them)
+    if (!IsBF16<CODE>::value && tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(sh.dlt));
     uint4 ck = make_uint4(0, 0, 0, 0), cu = make_uint4(0, 0, 0, 0);
     if (ts < a.n_comp) {
         const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
@@ -709,16 +743,17 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
     }
 
     // ---- quantized residual -------------------------------------------------------
-    if (CODE == 1) {
+    if (CODE == 1 || CODE == 4) {
         // thread (v, h) takes half h of code row v
         const int v = tid >> 1, h = tid & 1;
         double zk;
         float zq;
-        code_product_e4m3<CODE, KS>(sh, v, h, zk, zq);
+        if (CODE == 4) code_product_bf16<CODE, KS>(sh, v, h, zk, zq);
+        else code_product_e4m3<CODE, KS>(sh, v, h, zk, zq);
         if (KS) zk += dpp<DPP_XOR1>(zk);
         zq += dpp<DPP_XOR1>(zq);
         if (h == 0) {
-            const float dl = sh.dlt[v];
+            const float dl = IsBF16<CODE>::value ? 1.0f : sh.dlt[v];
             if (KS) sh.zk[POS(v)] = (double)dl * zk;
             sh.zq[POS(v)] = dl * zq;
         }

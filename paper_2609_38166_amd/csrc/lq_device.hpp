@@ -149,6 +149,12 @@ template <> struct CodeFmt<0> { static constexpr int BITS = 8; static constexpr 
 template <> struct CodeFmt<1> { static constexpr int BITS = 8; static constexpr float QMAX = 448.0f; };
 template <> struct CodeFmt<2> { static constexpr int BITS = 4; static constexpr float QMAX = 7.0f; };
 template <> struct CodeFmt<3> { static constexpr int BITS = 6; static constexpr float QMAX = 31.0f; };
+// CODE 4: the state itself in BF16 (the per-window BF16 variant): unit scales,
+// no smoothing, no Compensator Tokens.
+template <> struct CodeFmt<4> { static constexpr int BITS = 16; static constexpr float QMAX = 1.0f; };
+
+// CODE 4 stores BF16 state values; every other code is an integer or an E4M3 byte.
+template <int CODE> struct IsBF16 { static constexpr bool value = CODE == 4; };
 
 // Signed field of `bits` bits at bit `off` of w (off + bits <= 32).
 __device__ __forceinline__ int32_t sfield(uint32_t w, int off, int bits) {

@@ -60,6 +60,7 @@ hipError_t launch_decode_commit(const lq_dims &d, const StatePtrs &s, const Toke
             case LQ_CODE_E4M3: return launch<1, 1>(a, c, d.rule, st);
             case LQ_CODE_INT4: return launch<1, 2>(a, c, d.rule, st);
             case LQ_CODE_INT6: return launch<1, 3>(a, c, d.rule, st);
+            case LQ_CODE_BF16: return launch<1, 4>(a, c, d.rule, st);
             default: return launch<1, 0>(a, c, d.rule, st);
         }
     }
@@ -67,6 +68,7 @@ hipError_t launch_decode_commit(const lq_dims &d, const StatePtrs &s, const Toke
         case LQ_CODE_E4M3: return launch<0, 1>(a, c, d.rule, st);
         case LQ_CODE_INT4: return launch<0, 2>(a, c, d.rule, st);
         case LQ_CODE_INT6: return launch<0, 3>(a, c, d.rule, st);
+        case LQ_CODE_BF16: return launch<0, 4>(a, c, d.rule, st);
         default: return launch<0, 0>(a, c, d.rule, st);
     }
 }

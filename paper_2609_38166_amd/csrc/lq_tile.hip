@@ -38,6 +38,7 @@ hipError_t launch_tile(const lq_dims &d, const StatePtrs &s, int mode, const flo
             case LQ_CODE_E4M3: return launch2<1, 1>(a, tiles, mode, st);
             case LQ_CODE_INT4: return launch2<1, 2>(a, tiles, mode, st);
             case LQ_CODE_INT6: return launch2<1, 3>(a, tiles, mode, st);
+            case LQ_CODE_BF16: return launch2<1, 4>(a, tiles, mode, st);
             default: return launch2<1, 0>(a, tiles, mode, st);
         }
     }
@@ -45,6 +46,7 @@ hipError_t launch_tile(const lq_dims &d, const StatePtrs &s, int mode, const flo
         case LQ_CODE_E4M3: return launch2<0, 1>(a, tiles, mode, st);
         case LQ_CODE_INT4: return launch2<0, 2>(a, tiles, mode, st);
         case LQ_CODE_INT6: return launch2<0, 3>(a, tiles, mode, st);
+        case LQ_CODE_BF16: return launch2<0, 4>(a, tiles, mode, st);
         default: return launch2<0, 0>(a, tiles, mode, st);
     }
 }

@@ -55,15 +55,39 @@ __device__ __forceinline__ constexpr int KP(int kb, int a) { return 16 * a + kb;
 __device__ __forceinline__ constexpr int KCH(int t) { return 8 * (t & 15) + (t >> 4); }
 
 // The 8 codes of row v (value channel), key channels 8kb..8kb+7: 8 bytes for
-// the byte formats, 4 for INT4, 6 (three 16-bit words) for INT6.
+// the byte formats, 4 for INT4, 6 (three 16-bit words) for INT6, 16 (eight
+// BF16 values) for the BF16 state.
+template <int CODE> struct Codes8 { typedef uint2 type; };
+template <> struct Codes8<4> { typedef uint4 type; };
+
 template <int CODE>
-__device__ __forceinline__ uint2 load_codes8(const uint8_t *codes, int tile, int v, int kb) {
+__device__ __forceinline__ typename Codes8<CODE>::type load_codes8(const uint8_t *codes, int tile, int v, int kb) {
     constexpr int ROW = D * CodeFmt<CODE>::BITS / 8;
     const uint8_t *p = codes + ((size_t)tile * D + v) * ROW + kb * CodeFmt<CODE>::BITS;
-    if (CODE <= 1) return *(const uint2 *)p;
-    if (CODE == 2) return make_uint2(*(const uint32_t *)p, 0u);
-    const uint16_t *h = (const uint16_t *)p;
-    return make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2]);
+    typename Codes8<CODE>::type w;
+    if constexpr (CODE == 4) {
+        w = *(const uint4 *)p;
+    } else if constexpr (CODE <= 1) {
+        w = *(const uint2 *)p;
+    } else if constexpr (CODE == 2) {
+        w = make_uint2(*(const uint32_t *)p, 0u);
+    } else {
+        const uint16_t *h = (const uint16_t *)p;
+        w = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2]);
+    }
+    return w;
+}
+
+// Value a (0..7) of the 8 codes as a double (BF16 state: the value itself).
+template <int CODE>
+__device__ __forceinline__ double code8_value(const typename Codes8<CODE>::type &z, int a) {
+    if constexpr (CODE == 4) {
+        const uint32_t x = a < 2 ? z.x : a < 4 ? z.y : a < 6 ? z.z : z.w;
+        return (double)bf2f((uint16_t)(x >> (16 * (a & 1))));
+    } else {
+        const uint32_t w[2] = {z.x, z.y};
+        return (double)code_at<CODE>(w, a);
+    }
 }
 
 template <int CODE>
@@ -222,13 +246,16 @@ __device__ __forceinline__ void tile_body(const TileArgs &A, TileShared &sh, int
         // first pass of records.
         const int p = p_given >= 0 ? p_given : A.rec_len[tile];
         const int l16 = tid & 15, ts = tid >> 4;    // staging: segment, slot
-        uint2 zp[VPT];
+        typename Codes8<CODE>::type zp[VPT];
 #pragma unroll
         for (int b = 0; b < VPT; ++b) zp[b] = load_codes8<CODE>(A.codes, tile, VPT * vb + b, kb);
-        const float4 dl0 = *(const float4 *)(A.scale + tvec + VPT * vb);
-        const float4 dl1 = *(const float4 *)(A.scale + tvec + VPT * vb + 4);
-        const float4 c0 = *(const float4 *)(A.smooth + tvec + 8 * kb);
-        const float4 c1 = *(const float4 *)(A.smooth + tvec + 8 * kb + 4);
+        // (the BF16 state has unit scales and no smoothing; its arrays are not read)
+        const float4 one4 = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+        const bool bf = IsBF16<CODE>::value;
+        const float4 dl0 = bf ? one4 : *(const float4 *)(A.scale + tvec + VPT * vb);
+        const float4 dl1 = bf ? one4 : *(const float4 *)(A.scale + tvec + VPT * vb + 4);
+        const float4 c0 = bf ? one4 : *(const float4 *)(A.smooth + tvec + 8 * kb);
+        const float4 c1 = bf ? one4 : *(const float4 *)(A.smooth + tvec + 8 * kb + 4);
         uint4 ck = make_uint4(0, 0, 0, 0), cu = ck;
         if (ts < r) {
             ck = *(const uint4 *)(A.comp_k + ((size_t)tile * r + ts) * D + 8 * l16);
@@ -279,10 +306,9 @@ __device__ __forceinline__ void tile_body(const TileArgs &A, TileShared &sh, int
             const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
 #pragma unroll
             for (int b = 0; b < VPT; ++b) {
-                const uint32_t w[2] = {zp[b].x, zp[b].y};
 #pragma unroll
                 for (int a = 0; a < 8; ++a) {
-                    const double zf = (double)code_at<CODE>(w, a);
+                    const double zf = code8_value<CODE>(zp[b], a);
                     m[a][b] = (double)cv[a] * (zf * (double)dv[b]);
                 }
             }
@@ -507,6 +533,26 @@ __device__ __forceinline__ void tile_body(const TileArgs &A, TileShared &sh, int
         }
     }
 
+    if constexpr (IsBF16<CODE>::value) {
+        // BF16 state: every entry rounded to nearest even through fp32 (the
+        // window-end rounding of the per-window BF16 variant), unit scales
+        refresh();
+        constexpr int ROW = D * 2;
+#pragma unroll
+        for (int b = 0; b < VPT; ++b) {
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                w[e] = (uint32_t)f2bf((float)m[2 * e][b]) | ((uint32_t)f2bf((float)m[2 * e + 1][b]) << 16);
+            *(uint4 *)(A.codes + ((size_t)tile * D + VPT * vb + b) * ROW + 16 * kb) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+        if (tid < D) {
+            A.smooth[tvec + tid] = 1.0f;
+            A.scale[tvec + tid] = 1.0f;
+        }
+        if (tid == 0) A.rec_len[tile] = 0;
+        return;
+    }
     refresh();
     // residual smoothing over key rows: c_k = sqrt(max(mean_v |R_kv|, 1e-12)) in fp32
     {

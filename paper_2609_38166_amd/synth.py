@@ -30,7 +30,7 @@ from dataclasses import dataclass, field, replace
 import numpy as np
 
 GATE_SCALAR, GATE_DIAG = 0, 1
-CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6 = 0, 1, 2, 3
+CODE_INT8, CODE_E4M3, CODE_INT4, CODE_INT6, CODE_BF16 = 0, 1, 2, 3, 4
 PHASE_PREFILL, PHASE_DECODE, PHASE_OUTLIER = 0, 1, 2
 
 
@@ -84,6 +84,9 @@ WORKLOADS = {
 # the KDA layer with the lower-bit residual codes (same inputs, r = 8)
 WORKLOADS["kda_kimi_int4"] = WORKLOADS["kda_kimi"].with_(name="kda_kimi_int4", code=CODE_INT4)
 WORKLOADS["kda_kimi_int6"] = WORKLOADS["kda_kimi"].with_(name="kda_kimi_int6", code=CODE_INT6)
+# the per-window BF16 state (no Compensator Tokens, no smoothing) at the headline shape
+WORKLOADS["kda_kimi_bf16w"] = WORKLOADS["kda_kimi"].with_(name="kda_kimi_bf16w", code=CODE_BF16, n_comp=0,
+                                                          smooth=0)
 
 
 def _threads(n=None) -> int:

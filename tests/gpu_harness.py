@@ -70,6 +70,10 @@ def gdims(wl: synth.Workload, **kw) -> B.lq_dims:
 
 def code_ordinal(Z, code):
     """Position of each code on the ordered grid of representable values."""
+    if code == synth.CODE_BF16:
+        b = np.asarray(Z, np.uint16).astype(np.int64)
+        mag = b & 0x7FFF
+        return np.where(b & 0x8000, -mag, mag)
     Z = np.asarray(Z, np.uint8)
     if code != synth.CODE_E4M3:
         return Z.view(np.int8).astype(np.int64)
@@ -86,14 +90,16 @@ def code_agreement(Zg, Zo, code):
 
 # --------------------------------------------------------------------------- representation I/O
 
-CODE_BITS = {synth.CODE_INT8: 8, synth.CODE_E4M3: 8, synth.CODE_INT4: 4, synth.CODE_INT6: 6}
+CODE_BITS = {synth.CODE_INT8: 8, synth.CODE_E4M3: 8, synth.CODE_INT4: 4, synth.CODE_INT6: 6, synth.CODE_BF16: 16}
 
 
 def pack_codes(Zt, code):
     """[n][rows][128] code bytes (one code per byte, two's complement for the
     integer formats) to the library's row layout: INT4 two per byte (even
     channel low), INT6 four per three bytes (channel 4i+q at bits 6q of the
-    little-endian 24-bit group i)."""
+    little-endian 24-bit group i).  The BF16 state: its 16-bit values as bytes."""
+    if code == synth.CODE_BF16:
+        return np.ascontiguousarray(np.asarray(Zt, np.uint16)).view(np.uint8)
     Zt = np.asarray(Zt, np.uint8)
     if CODE_BITS[code] == 8:
         return Zt
@@ -109,7 +115,10 @@ def pack_codes(Zt, code):
 
 
 def unpack_codes(P, code, n_ch=128):
-    """Inverse of pack_codes: one two's-complement code per byte."""
+    """Inverse of pack_codes: one two's-complement code per byte (BF16 bits for
+    the BF16 state)."""
+    if code == synth.CODE_BF16:
+        return np.ascontiguousarray(np.asarray(P, np.uint8)).view(np.uint16)
     P = np.asarray(P, np.uint8)
     if CODE_BITS[code] == 8:
         return P
@@ -134,7 +143,7 @@ def upload_rep(st: B.State, idx, Z, delta, c, Kt, Ut):
     n, dk, dv, r = len(idx), dims.d_k, dims.d_v, dims.n_comp
     idx_t = torch.as_tensor(np.asarray(idx, np.int64), device="cuda")
     rowb = dk * CODE_BITS[dims.code] // 8
-    st.codes.view(-1, dv, rowb)[idx_t] = dev(pack_codes(np.asarray(Z, np.uint8).transpose(0, 2, 1), dims.code))
+    st.codes.view(-1, dv, rowb)[idx_t] = dev(pack_codes(np.asarray(Z).transpose(0, 2, 1), dims.code))
     st.scale.view(-1, dv)[idx_t] = dev(np.asarray(delta, np.float32))
     st.smooth.view(-1, dk)[idx_t] = dev(np.asarray(c, np.float32))
     if r:

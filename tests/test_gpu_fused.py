@@ -30,6 +30,8 @@ PARITY = {
     "kda_int4_small": W_["kda_kimi"].with_(name="kda_int4_small", batch=2, heads_v=4, heads_k=4, steps=64,
                                            window=32, prefill=128, code=synth.CODE_INT4),
     "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1, steps=32),
+    "bf16w_kda": W_["kda_kimi"].with_(name="bf16w_kda", batch=2, heads_v=4, heads_k=4, steps=64, window=16,
+                                      prefill=128, code=synth.CODE_BF16, n_comp=0, smooth=0),
 }
 
 

@@ -59,6 +59,12 @@ SMALL = {
     "mamba2_int4": W_["gdn_tiny"].with_(name="mamba2_int4", rule=1, code=synth.CODE_INT4, n_comp=8),
     "gla_int6": W_["kda_kimi"].with_(name="gla_int6", batch=2, heads_v=4, heads_k=4, steps=64, window=32,
                                      n_comp=4, prefill=128, rule=1, code=synth.CODE_INT6),
+    # the per-window BF16 state (row f3): BF16 rounding at window ends, no tokens
+    "bf16w_gdn": W_["gdn_tiny"].with_(name="bf16w_gdn", code=synth.CODE_BF16, n_comp=0, smooth=0),
+    "bf16w_kda": W_["kda_kimi"].with_(name="bf16w_kda", batch=2, heads_v=4, heads_k=4, steps=128, window=32,
+                                      prefill=256, code=synth.CODE_BF16, n_comp=0, smooth=0),
+    "bf16w_gqa_w1": W_["gdn_qwen3next"].with_(name="bf16w_gqa_w1", batch=2, heads_v=4, heads_k=2, steps=12,
+                                              window=1, prefill=64, code=synth.CODE_BF16, n_comp=0, smooth=0),
 }
 
 
@@ -179,7 +185,31 @@ def test_quantize_state_parity(code, r, smooth):
     assert got["delta"][2][5] == 0 and got["delta"][2][99] == 0
 
 
-@pytest.mark.parametrize("name", ["gdn_tiny", "kda_small", "gqa_e4m3_small", "kda_int4_small", "gdn_int6_small"])
+def test_quantize_state_parity_bf16():
+    """The BF16 state: quantization is the BF16 rounding of every entry (edge
+    tiles included), bit for bit."""
+    wl = W_["gdn_tiny"].with_(batch=4, heads_v=8, heads_k=8, n_comp=0, code=synth.CODE_BF16, smooth=0)
+    S = _states_with_edges(wl.tiles, 150)
+    S[0, 0, :8] = np.float32([1e-39, -3e-40, 0.0, -0.0, 1e-45, 3.0e38, -1.17e-38, 7e-39])
+    cfg = H.ocfg(wl)
+    exp = {"Z": [], "delta": [], "c": [], "Kt": [], "Ut": []}
+    for i in range(wl.tiles):
+        rep = O.quantize(cfg, S[i])
+        for k_ in exp:
+            exp[k_].append(getattr(rep, k_))
+    exp = {k_: np.stack(v_) for k_, v_ in exp.items()}
+    dims = H.gdims(wl)
+    st = B.State.empty(dims)
+    st.rec_len.fill_(3)
+    B.leapquant_quantize_state(dims, H.dev(S.transpose(0, 2, 1).astype(np.float32)), st)
+    got = H.download_rep(st)
+    assert np.all(got["rec_len"] == 0)
+    assert np.array_equal(got["Z"], exp["Z"])
+    assert np.all(got["delta"] == 1.0) and np.all(got["c"] == 1.0)
+
+
+@pytest.mark.parametrize("name", ["gdn_tiny", "kda_small", "gqa_e4m3_small", "kda_int4_small", "gdn_int6_small",
+                                  "bf16w_kda"])
 def test_dequantize_state_parity(name):
     """Base + open-window records, materialised on the GPU from the oracle's
     representation and records, equals the oracle's dense window state."""
@@ -538,6 +568,7 @@ FULL = {
     "gdn_long": (W_["gdn_long"], 24, 1),
     "kda_kimi_int4": (W_["kda_kimi_int4"], 32, 1),
     "kda_kimi_int6": (W_["kda_kimi_int6"], 32, 1),
+    "kda_kimi_bf16w": (W_["kda_kimi_bf16w"], 32, 1),
 }
 
 
