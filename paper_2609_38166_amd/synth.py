@@ -11,7 +11,8 @@ whose weights and datasets are not available), all computed in float32:
   v     ~ N(0, I_d);
   beta  = sigmoid(N(0, 1));
   decay = exp(-0.1 * softplus(N(0, 1))): one scalar per token for the scalar
-          gate, d_k independent draws per token for the per-channel gate.
+          gate, d_k independent draws per token for the per-channel gate
+          (Workload.gate_scale replaces 0.1 for a long-memory variant).
 
 Every tile (request b, value head h) owns two independent PCG64 streams seeded
 from SeedSequence([seed, phase, kind, b, head]): kind 0 is the key stream of
@@ -53,6 +54,7 @@ class Workload:
     rule: int = 0             # read vector: delta rule (0), b_t = 0 (1), given with the token (2)
     outliers: str = "all"     # "all": every tile; "frac": 5 % of tiles; "none"
     outlier_factor: float = 20.0
+    gate_scale: float = 0.1           # decay = exp(-gate_scale * softplus(N(0, 1)))
     seed: int = 20260000
     extra: dict = field(default_factory=dict)
 
@@ -158,7 +160,7 @@ class Streams:
             za = buf[:, :, wl.dv + 1:]
             # softplus(z) = max(z, 0) + log1p(exp(-|z|))
             sp = np.maximum(za, np.float32(0.0)) + np.log1p(np.exp(-np.abs(za)))
-            alpha[:, lo:hi] = np.exp(np.float32(-0.1) * sp).transpose(1, 0, 2)
+            alpha[:, lo:hi] = np.exp(np.float32(-wl.gate_scale) * sp).transpose(1, 0, 2)
 
         def spans(total, per=64):
             return [(lo, min(lo + per, total)) for lo in range(0, total, per)]
