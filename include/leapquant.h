@@ -82,7 +82,7 @@ extern "C" {
 /* Limits of this version. */
 #define LQ_MAX_COMP        16
 #define LQ_MAX_WINDOW_GDN 256
-#define LQ_MAX_WINDOW_KDA  64
+#define LQ_MAX_WINDOW_KDA 256
 #define LQ_MAX_POWER_ITERS 64
 /* Also: batch * heads_v <= 2^30 and batch * heads_v * (heads_v / heads_k) < 2^32
  * (LQ_EUNSUPPORTED otherwise). */

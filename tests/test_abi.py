@@ -95,7 +95,7 @@ def test_validation_rejects_bad_arguments_before_launch():
                      ({"n_comp": -1}, B.LQ_EINVAL),
                      ({"gate": 2}, B.LQ_EINVAL), ({"code": 5}, B.LQ_EINVAL),
                      ({"n_comp": 2, "power_iters": 0}, B.LQ_EUNSUPPORTED),
-                     ({"window": 65, "gate": B.LQ_GATE_DIAG}, B.LQ_EUNSUPPORTED)]:
+                     ({"window": 257, "gate": B.LQ_GATE_DIAG}, B.LQ_EUNSUPPORTED)]:
         dd = B.make_dims(2, 4, heads_k=2, **kw)
         assert _call_decode(dd, st, toks) == code, kw
     assert _call_decode(B.make_dims(2, 4, heads_k=3), st, toks) == B.LQ_EINVAL

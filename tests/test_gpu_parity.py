@@ -49,6 +49,12 @@ SMALL = {
     # ragged tile count (3 requests x 5 heads)
     "gdn_w256": W_["gdn_tiny"].with_(name="gdn_w256", batch=2, heads_v=2, heads_k=2, steps=256, window=256,
                                      prefill=128),
+    # the largest windows of the per-channel gate: three and six record passes of 48 in
+    # the decode, eight and sixteen passes of 16 in the commit
+    "kda_w128": W_["kda_kimi"].with_(name="kda_w128", batch=1, heads_v=4, heads_k=4, steps=256, window=128,
+                                     prefill=128),
+    "kda_w256": W_["kda_kimi"].with_(name="kda_w256", batch=1, heads_v=2, heads_k=2, steps=256, window=256,
+                                     prefill=128),
     "ragged_3x5": W_["gdn_tiny"].with_(name="ragged_3x5", batch=3, heads_v=5, heads_k=5, steps=48, prefill=128),
     # b_t = 0 rows of the instance table: Mamba2 (scalar decay), GLA / RWKV6 (per-channel)
     "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1),
