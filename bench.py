@@ -59,7 +59,8 @@ def parse():
                          "0.001: a long-memory variant)")
     ap.add_argument("--profile-decode", action="store_true",
                     help="short run for profilers: setup, then the decode with rotating batches (the "
-                         "roofline timing) and one device copy for calibrating byte counters")
+                         "roofline timing), eight steps of each dense baseline and one device copy for "
+                         "calibrating byte counters")
     return ap.parse_args()
 
 
@@ -675,6 +676,43 @@ def copy_calibration(nbytes=1 << 30):
     del src, dst
 
 
+def stream_rw_ceiling(nbytes, reps=5):
+    """Measured HBM rate (bytes read + bytes written per second) of a kernel
+    that reads a buffer and writes it back in place with coalesced 16-byte
+    plain loads and stores, nothing else: the ceiling of the dense baselines'
+    access pattern at the same state size."""
+    import ctypes as C
+    import torch
+    from paper_2609_38166_amd import build as lib_build
+    L = C.CDLL(lib_build.BENCH_LIB)
+    L.lqb_stream_rw.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_void_p]
+    L.lqb_stream_rw.restype = C.c_int
+    buf = torch.zeros(nbytes // 4, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    best = None
+    for grid in (256 * 16, 256 * 64, 256 * 256):
+        def launch():
+            rc = L.lqb_stream_rw(buf.data_ptr(), nbytes, grid, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"lqb_stream_rw failed: {rc}")
+        launch()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        gbs = 2 * nbytes / float(np.median(ts)) / 1e9
+        if best is None or gbs > best["gbps"]:
+            best = {"gbps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes,
+                    "grid": grid}
+    del buf
+    return best
+
+
 def stream_read_ceiling(nbytes=4 << 30, reps=5):
     """Measured HBM read rate of a kernel that only streams a 4 GiB buffer
     (non-temporal 16-byte coalesced loads, far beyond the 256 MB Infinity
@@ -709,12 +747,23 @@ def stream_read_ceiling(nbytes=4 << 30, reps=5):
     return {"gbps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes}
 
 
+DECODE_SOURCES = ("lq_decode.hip", "lq_decode.hpp", "lq_device.hpp")
+
+
+def decode_source_sha():
+    """sha256 over the decode kernel's sources (launch, body, device helpers), in that order."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in DECODE_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2609_38166_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def traffic_from_profile(wl):
     """HBM bytes per decode launch from the committed counter summary, if it
     was taken on the current decode kernel source; None otherwise."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"decode_step_traffic_{wl.name}.md")
-    src = os.path.join(ROOT, "paper_2609_38166_amd", "csrc", "lq_decode.hip")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -722,8 +771,7 @@ def traffic_from_profile(wl):
         if ":" in line and line.startswith("- "):
             key, val = line[2:].split(":", 1)
             fields[key.strip()] = val.strip().strip("`")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if fields.get("lq_decode.hip sha256") != sha or "traffic bytes per launch" not in fields:
+    if fields.get("decode source sha256") != decode_source_sha() or "traffic bytes per launch" not in fields:
         return None
     return float(fields["traffic bytes per launch"])
 
@@ -905,6 +953,15 @@ def main():
     if args.profile_decode:
         ncold = cold_copies(wl)
         cold = decode_rotating(wl, dims, S0, toks, copies=ncold, reps=2)
+        # eight steps of each dense baseline, for their counters
+        q, k, v, a, b = toks
+        for dtype, tdt in ((B_.LQ_STATE_F32, torch.float32), (B_.LQ_STATE_BF16, torch.bfloat16)):
+            S = S0.to(tdt).contiguous()
+            o = torch.empty((wl.batch, wl.heads_v, wl.dv), dtype=torch.float32, device="cuda")
+            for t in range(8):
+                B_.leapquant_baseline_step(dims, S, dtype, q[t], k[t], v[t], a[t], b[t], o)
+            torch.cuda.synchronize()
+            del S
         copy_calibration()
         print(json.dumps({"profile_decode_us": round(cold * 1e3, 2), "rotating_batches": ncold}), flush=True)
         return
@@ -1096,8 +1153,12 @@ def main():
             gbs = baseline_bytes(wl, width) * tile_steps * args.steps / bs / 1e9
             res[name] = {"value": round(rate, 1), "ms_per_step": round(bs / args.steps * 1e3, 4),
                          "effective_gbps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
-            log(f"[bench] {name} baseline {res[name]}")
             del S
+            torch.cuda.empty_cache()
+            rw = stream_rw_ceiling(wl.tiles * wl.dk * wl.dv * width)
+            res[name]["rw_ceiling_gbps"] = rw["gbps"]
+            res[name]["frac_of_rw_ceiling"] = round(gbs / rw["gbps"], 4)
+            log(f"[bench] {name} baseline {res[name]}")
         out["baselines"] = res
         out["speedup_vs_bf16"] = round(value / res["bf16"]["value"], 3)
         out["speedup_vs_fp32"] = round(value / res["fp32"]["value"], 3)

@@ -551,6 +551,9 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
         if ((tid & 63) == 0) sh.kq[tid >> 6] = kq;
         kx = xk;                                             // the base vectors read these
         qx = xq;
+        // parked in LDS until the first scan (or the base vectors) reads it back,
+        // so that no register holds it across the record loads
+        sh.yk[tid] = (double)carry0;
     }
 
     // partial readouts of this thread's slot, k side and q side (defined after
@@ -591,7 +594,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
     auto scan = [&](bool first) {
         // slot 0 holds the newest block
         if (tid < D) {
-            double c = first ? (double)carry0 : carry;
+            double c = first ? sh.yk[tid] : carry;
             // slot products read ahead of the chain (eight at a time), then
             // overwritten
 #pragma unroll
@@ -711,7 +714,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
         }
     } else {
         // ---- no records: base read vectors only ----
-        if (tid < D) base_vectors<CODE, KS>(sh, (double)carry0, kx, qx, cs, tid);
+        if (tid < D) base_vectors<CODE, KS>(sh, sh.yk[tid], kx, qx, cs, tid);
         wait_vm_all();
         __syncthreads();
 #pragma unroll

@@ -156,9 +156,9 @@ __device__ __forceinline__ double sum_parts(TileShared &sh) {
     double s = 0.0;
     const int t = threadIdx.x;
     if (t < D) {
-        double v[4] = {0.0, 0.0, 0.0, 0.0};
+        double v[4] = {sh.part[0][t], sh.part[1][t], sh.part[2][t], sh.part[3][t]};
 #pragma unroll
-        for (int j = 0; j < NVB; ++j) v[j & 3] += sh.part[j][t];
+        for (int j = 4; j < NVB; ++j) v[j & 3] += sh.part[j][t];
         s = (v[0] + v[1]) + (v[2] + v[3]);
     }
     return s;
@@ -197,9 +197,9 @@ __device__ __forceinline__ void row_sum8(TileShared &sh, double *v, int kb, int 
     for (int b = 0; b < 8; ++b) r[17 * b + kb] = v[b];
     __builtin_amdgcn_wave_barrier();
     const int c = kb & 7;
-    double t[4] = {0.0, 0.0, 0.0, 0.0};
+    double t[4] = {r[17 * c], r[17 * c + 1], r[17 * c + 2], r[17 * c + 3]};
 #pragma unroll
-    for (int l = 0; l < 16; ++l) t[l & 3] += r[17 * c + l];
+    for (int l = 4; l < 16; ++l) t[l & 3] += r[17 * c + l];
     if (kb < 8) r[17 * c + 16] = ((t[0] + t[1]) + (t[2] + t[3])) * scale;
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -464,11 +464,11 @@ __device__ __forceinline__ void tile_body(const TileArgs &A, TileShared &sh, int
             for (int b = 0; b < VPT; ++b) y[b] = 0.0;
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
-                const double xa = sh.vec[KP(kb, a)] * xs;
+                const double xa = sh.vec[KP(kb, a)];
 #pragma unroll
                 for (int b = 0; b < VPT; ++b) y[b] = fma(m[a][b], xa, y[b]);
             }
-            row_sum8(sh, y, kb, vb, sc);            // y_v = sc * sum_k M_kv x_k
+            row_sum8(sh, y, kb, vb, sc * xs);       // y_v = sc * sum_k M_kv (xs x_k)
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
                 double s = 0.0;
