@@ -211,14 +211,23 @@ __device__ __forceinline__ uint32_t int6x4_to_bytes(uint32_t g) {
     return ((t ^ 0x20202020u) + 0x60606060u) ^ 0x80808080u;
 }
 
+// A pass [lo, hi) of records, newest first, is dealt to the slots in
+// contiguous blocks of d = ceil((hi - lo) / SLOTS) <= PER_SLOT: slot ts takes
+// offsets d ts .. d ts + d - 1, so a short pass spreads over every slot and
+// its walk is d records deep.  Record q of slot ts, or -1.
+__device__ __forceinline__ int slot_record(int lo, int hi, int d, int ts, int q) {
+    const int j = d * ts + q;
+    return q < d && j < hi - lo ? hi - 1 - j : -1;
+}
+
 template <int GATE>
-__device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi,
+__device__ __forceinline__ void load_records(const DecodeArgs &a, size_t rbase, int lo, int hi, int d,
                                              int ts, int l16, RecRegs<GATE> &R) {
     constexpr int PER_SLOT = Pass<GATE>::PER_SLOT;
 #pragma unroll
     for (int q = 0; q < PER_SLOT; ++q) {
-        const int r = hi - 1 - (PER_SLOT * ts + q);
-        if (r >= lo) {
+        const int r = slot_record(lo, hi, d, ts, q);
+        if (r >= 0) {
             R.k[q] = ld_stream16(a.rec_k + (rbase + r) * D + 8 * l16);
             R.u[q] = ld_stream16(a.rec_u + (rbase + r) * D + 8 * l16);
             if (GATE) R.a[q] = ld_stream16(a.rec_a + (rbase + r) * D + 8 * l16);
@@ -523,7 +532,8 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
     RecRegs<GATE> R;
     constexpr int PER_SLOT = Pass<GATE>::PER_SLOT, PASS = Pass<GATE>::N;
     int hi = n, lo = n > PASS ? n - PASS : 0;
-    load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
+    int d = (hi - lo + SLOTS - 1) / SLOTS;
+    load_records<GATE>(a, rbase, lo, hi, d, ts, l16, R);
     // Nothing that consumes the token inputs may be scheduled above this point:
     // a wait for one of them ahead of the code and record loads would delay
     // every load of the tile by a memory round trip.
@@ -570,7 +580,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             for (int j = 0; j < 8; ++j) bp[j] = 1.0;
 #pragma unroll
             for (int q = 0; q < PER_SLOT; ++q) {
-                if (hi - 1 - (PER_SLOT * ts + q) >= lo) {
+                if (slot_record(lo, hi, d, ts, q) >= 0) {
                     const uint32_t w4[4] = {R.a[q].x, R.a[q].y, R.a[q].z, R.a[q].w};
 #pragma unroll
                     for (int j = 0; j < 8; ++j) bp[j] *= h2d(w4[j >> 1], j & 1);
@@ -582,7 +592,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             double bp = 1.0;
 #pragma unroll
             for (int q = 0; q < PER_SLOT; ++q)
-                if (hi - 1 - (PER_SLOT * ts + q) >= lo) bp *= (double)h2f((uint16_t)R.as[q]);
+                if (slot_record(lo, hi, d, ts, q) >= 0) bp *= (double)h2f((uint16_t)R.as[q]);
             if (l16 == 0) sh.bp[ts][0] = bp;
         }
     };
@@ -627,7 +637,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             }
 #pragma unroll
             for (int q = 0; q < PER_SLOT; ++q) {
-                if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                if (slot_record(lo, hi, d, ts, q) < 0) break;    // uniform within the slot
                 float kv[8], uv[8], av[8];
                 unpack_h8(R.k[q], kv);
                 unpack_h8(R.u[q], uv);
@@ -663,7 +673,7 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             }
 #pragma unroll
             for (int q = 0; q < PER_SLOT; ++q) {
-                if (hi - 1 - (PER_SLOT * ts + q) < lo) break;    // uniform within the slot
+                if (slot_record(lo, hi, d, ts, q) < 0) break;    // uniform within the slot
                 float kv[8], uv[8];
                 unpack_h8(R.k[q], kv);
                 unpack_h8(R.u[q], uv);
@@ -704,7 +714,8 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             // reads of the decay array before the next scan's writes.
             hi = lo;
             lo = hi > PASS ? hi - PASS : 0;
-            load_records<GATE>(a, rbase, lo, hi, ts, l16, R);
+            d = (hi - lo + SLOTS - 1) / SLOTS;
+            load_records<GATE>(a, rbase, lo, hi, d, ts, l16, R);
             block_products();
             __syncthreads();
             scan(false);
