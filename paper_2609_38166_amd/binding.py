@@ -13,7 +13,9 @@ from dataclasses import dataclass
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libleapquant.so")
+# The library; LEAPQUANT_LIB may name another build of it (a measurement
+# variant made by build.py), which must export the same symbols.
+LIB_PATH = os.environ.get("LEAPQUANT_LIB") or os.path.join(_PKG, "libleapquant.so")
 
 LQ_OK, LQ_EINVAL, LQ_EALIGN, LQ_EUNSUPPORTED, LQ_EHIP, LQ_EDEVICE = 0, -1, -2, -3, -4, -5
 LQ_GATE_SCALAR, LQ_GATE_DIAG = 0, 1

@@ -29,9 +29,15 @@ def sources():
     return sorted(glob.glob(os.path.join(PKG, "csrc", "*.hip")))
 
 
-def _compile(srcs, out, verbose):
+# A build-time alternative of the library, for measuring one design choice
+# against its alternative (never loaded unless named in LEAPQUANT_LIB):
+# the decode's integer code product on the vector ALU instead of the matrix cores.
+VALU_CP_LIB = os.path.join(PKG, "libleapquant_valucp.so")
+
+
+def _compile(srcs, out, verbose, defines=()):
     tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
+    cmd = [HIPCC, *FLAGS, *defines, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
            *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
@@ -45,5 +51,13 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_valu_code_product(verbose: bool = False) -> str:
+    _compile(sources(), VALU_CP_LIB, verbose, defines=("-DLQ_CODE_PRODUCT_VALU",))
+    return VALU_CP_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if "--valu-code-product" in sys.argv:
+        print(build_valu_code_product(verbose=True))
+    else:
+        print(build(verbose=True))

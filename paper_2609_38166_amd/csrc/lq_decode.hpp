@@ -22,18 +22,19 @@
 // fp64, and the code product exact in integer arithmetic.  The read vector
 // w = c . Gamma x is written as a fixed-point number, an exponent per 64
 // channels and five base-128 digits (34 bits, each digit an int8), and
-// Z^T w is a sum of int8 x int8 dot products (v_dot4_i32_i8) per digit,
-// combined in fp64 exactly.  The q side, which only feeds the output, uses
-// three digits and fp32.  E4M3 codes are not integers; their product is
-// taken in fp64 (k side) and fp32 (q side) on the vector ALU.
+// Z^T w is a sum of int8 x int8 products per digit, taken on the int8 matrix
+// cores (v_mfma_i32_16x16x64_i8, exact int32 sums) and combined in fp64
+// exactly.  The q side, which only feeds the output, uses three digits and
+// fp32.  E4M3 codes are not integers, and the BF16 state is not either; their
+// products are taken in fp64 (k side) and fp32 (q side) on the vector ALU.
 //
 // Every global load of the tile is issued before the first barrier: rec_len (a
 // scalar load, which the record loads wait for), the token inputs, the
 // d_v x d_k codes and row scales (copied straight into LDS, 16 bytes per lane
 // and instruction, so they hold no registers), the compensators, then one pass
 // of records, loaded non-temporally (16 slots of 16 lanes, each slot a
-// contiguous block of records, 16 bytes of key, correction and decay per
-// lane).  The decays Gamma_{j+1:i} are products of the FP16 record decays:
+// contiguous block of ceil(count / 16) records, 16 bytes of key, correction
+// and decay per lane).  The decays Gamma_{j+1:i} are products of the FP16 record decays:
 // each slot forms the product of its block, one scan over the 16 slots gives
 // every block the decay of all newer records, and the slot walks its block
 // from the newest record back.  No d_k x d_v intermediate exists.
@@ -397,6 +398,85 @@ __device__ __forceinline__ v4i codes_i8(const DecodeShared<CODE> &sh, int v, int
                (int)int6x4_to_bytes(__builtin_amdgcn_alignbit(w2, w1, 16) & 0xFFFFFFu),
                (int)int6x4_to_bytes(w2 >> 8)};
 }
+
+// The same product on the vector ALU (a build-time alternative, selected by
+// LQ_CODE_PRODUCT_VALU, kept to measure the matrix-core form against):
+// thread (v, h) takes half h of code row v, one v_dot4_i32_i8 per 4 channels
+// and digit, per exponent group g = (c >> 2) & 1; the digit sums are
+// combined like the matrix-core ones.
+#ifdef LQ_CODE_PRODUCT_VALU
+template <int CODE, bool KS>
+__device__ __forceinline__ void code_product_valu(const DecodeShared<CODE> &sh, int v, int h, double &zk,
+                                                  float &zq) {
+    constexpr int D0 = KS ? 0 : KDIG;            // first digit row used
+    const uint32_t *dig = (const uint32_t *)sh.rv;   // [NDIG][D / 4] words
+    int acc[NDIG][2];
+#pragma unroll
+    for (int d = 0; d < NDIG; ++d) acc[d][0] = acc[d][1] = 0;
+    // the 4-channel words of this half row as int8 bytes: word i holds
+    // channels 64h + 4i .. 64h + 4i + 3, exponent group i & 1
+    auto dot_word = [&](uint32_t zb, int i) {
+        const int g = i & 1;
+#pragma unroll
+        for (int d = D0; d < NDIG; ++d)
+            acc[d][g] = __builtin_amdgcn_sdot4((int)zb, (int)dig[d * (D / 4) + 16 * h + i], acc[d][g], false);
+    };
+    if (CODE == 0) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const uint4 z = lds_chunk<CODE>(sh.codes, v, 4 * h + m);
+            dot_word(z.x, 4 * m + 0);
+            dot_word(z.y, 4 * m + 1);
+            dot_word(z.z, 4 * m + 2);
+            dot_word(z.w, 4 * m + 3);
+        }
+    } else if (CODE == 2) {
+        // 32 codes per chunk, two chunks per half row; each word holds 8 channels
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const uint4 z = lds_chunk<CODE>(sh.codes, v, 2 * h + m);
+            const uint32_t zw[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                dot_word(int4x4_to_bytes(zw[p], 0), 8 * m + 2 * p);
+                dot_word(int4x4_to_bytes(zw[p], 1), 8 * m + 2 * p + 1);
+            }
+        }
+    } else {
+        // 48 bytes per half row, four units of 12 bytes = 4 groups of 3 bytes
+        const uint32_t *zr = (const uint32_t *)sh.codes + v * (Rows<CODE>::BYTES / 4) + 12 * h;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t w0 = zr[3 * u], w1 = zr[3 * u + 1], w2 = zr[3 * u + 2];
+            dot_word(int6x4_to_bytes(w0 & 0xFFFFFFu), 4 * u);
+            dot_word(int6x4_to_bytes(__builtin_amdgcn_alignbit(w1, w0, 24) & 0xFFFFFFu), 4 * u + 1);
+            dot_word(int6x4_to_bytes(__builtin_amdgcn_alignbit(w2, w1, 16) & 0xFFFFFFu), 4 * u + 2);
+            dot_word(int6x4_to_bytes(w2 >> 8), 4 * u + 3);
+        }
+    }
+    // sum_d acc_d 128^-d is exact in fp64 (|acc_d| < 2^19, 34 bits below)
+    double sk = 0.0;
+    if (KS) {
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+            double s = (double)acc[KDIG - 1][g];
+#pragma unroll
+            for (int d = KDIG - 2; d >= 0; --d) s = fma(s, 0x1p-7, (double)acc[d][g]);
+            sk += __builtin_ldexp(s, sh.ex[0][g] - 6);
+        }
+    }
+    float sq = 0.0f;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+        float s = (float)acc[NDIG - 1][g];
+#pragma unroll
+        for (int d = NDIG - 2; d >= KDIG; --d) s = fmaf(s, 0x1p-7f, (float)acc[d][g]);
+        sq += __builtin_ldexpf(s, sh.ex[1][g] - 6);
+    }
+    zk = sk;
+    zq = sq;
+}
+#endif
 
 // Integer code product of wave w's 32 rows on the integer matrix cores.  The
 // products are exact: every code and every digit is an int8, and the int32
@@ -772,7 +852,20 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
             sh.zq[POS(v)] = dl * zq;
         }
     } else {
+#ifdef LQ_CODE_PRODUCT_VALU
+        const int v = tid >> 1, h = tid & 1;
+        double zk;
+        float zq;
+        code_product_valu<CODE, KS>(sh, v, h, zk, zq);
+        if (KS) zk += dpp<DPP_XOR1>(zk);
+        zq += dpp<DPP_XOR1>(zq);
+        if (h == 0) {
+            if (KS) sh.zk[POS(v)] = (double)sh.dlt[v] * zk;
+            sh.zq[POS(v)] = sh.dlt[v] * zq;
+        }
+#else
         code_product_mfma<CODE, KS>(sh, tid);
+#endif
     }
 
     // sum over the wave's 4 slots in registers, then over the 4 waves in LDS:
