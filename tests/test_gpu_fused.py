@@ -32,6 +32,9 @@ PARITY = {
     "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1, steps=32),
     "bf16w_kda": W_["kda_kimi"].with_(name="bf16w_kda", batch=2, heads_v=4, heads_k=4, steps=64, window=16,
                                       prefill=128, code=synth.CODE_BF16, n_comp=0, smooth=0),
+    # a long per-channel-gate window: three record passes in the decode, eight in the fused commit
+    "kda_w128": W_["kda_kimi"].with_(name="kda_w128", batch=1, heads_v=4, heads_k=4, steps=256, window=128,
+                                     prefill=128),
 }
 
 
