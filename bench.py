@@ -1006,7 +1006,7 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
+        "dtype": "f32+f64", "data": "synthetic",
         "config": {"workload": f"{wl.name}: KDA (per-channel gate) batch {wl.batch}, {wl.heads_v} heads, "
                                f"d_k=d_v={wl.dk}, {wl.steps} decode tokens, W={wl.window}, "
                                f"r={wl.n_comp}, int8 state" if wl.gate == synth.GATE_DIAG else wl.name,
