@@ -22,8 +22,10 @@
  *    alignment.  So one step of a step-major token buffer, or a state whose
  *    arrays all start at the same tile of a larger one (a group of requests),
  *    can be passed for any tile count.
- *  - The library allocates no memory, keeps no global state and never
- *    synchronises (except leapquant_check_error).  Work is enqueued on
+ *  - The library allocates no memory, keeps no device state and never
+ *    synchronises (except leapquant_check_error).  Its only mutable state is
+ *    a per-thread buffer with the text of the last HIP error it saw
+ *    (leapquant_last_hip_error).  Work is enqueued on
  *    `stream` (a hipStream_t; NULL = the default stream) and returns at once.
  *    Calls on different streams with disjoint buffers may run concurrently
  *    (request groups of one state share only its error word, which the
@@ -154,6 +156,8 @@ int32_t leapquant_state_bytes(const lq_dims *dims, size_t bytes_out[10]);
  * delta_v = max_k |R^C_kv| / 127, code = clamp(rint(R^C * 127/max), +-127).
  * The 6- and 4-bit variants (the paper's lower-bit LeapQuant, Sec. 4.1-4.2)
  * use the same rule with qmax = 31 and 7 (2^(b-1) - 1) and packed storage.
+ * LQ_CODE_BF16 (per-window BF16, Sec. 3.2) stores every entry rounded to
+ * BF16 (nearest even) with unit scales and smoothing and no tokens.
  * The fit, the deflation and the smoothing statistic are carried in fp64;
  * the FP16 rounding of the tokens and the codes are decided in fp32.
  */
@@ -169,7 +173,10 @@ int32_t leapquant_quantize_state(const lq_dims *dims, const float *S, lq_state *
  *   A^T x = delta . (Z^T (c . Gamma_{1:i} x)) + U~ (K~^T Gamma_{1:i} x)
  *           + sum_{j<i} u_j (k~_j^T Gamma_{j+1:i} x)          for x = k, q
  *   u_i = fp16(v - A^T k),  k~_i = fp16(beta k),  o = A^T q + u_i (k~_i . q)
- * and the record (alpha_i, k~_i, u_i) is appended; rec_len += 1.  A tile whose
+ * and the record (alpha_i, k~_i, u_i) is appended; rec_len += 1.  Everything
+ * that feeds u_i (A^T k) is evaluated at fp64 accuracy, the code product
+ * exactly, so u_i is the correctly rounded FP16 value; the q side is fp32.
+ * k~_i is beta k rounded to fp32 and then to FP16.  A tile whose
  * rec_len already equals W is not modified: its o is NaN and
  * LQ_DEVERR_WINDOW_FULL is raised in *err.  dims->rule LQ_RULE_GENERAL is
  * rejected (LQ_EINVAL): that rule takes its read vectors through
