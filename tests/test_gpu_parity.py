@@ -249,16 +249,18 @@ def test_window_synchronised_parity(name):
     H.window_sync_parity(wl)
 
 
-def test_free_running_tiny():
-    """The whole GDN tiny trajectory on the GPU alone: from the oracle's fp32
-    initial state, its own quantization, 256 decode steps and 16 commits of its
-    own records, with nothing handed back from the oracle.  Every output and
-    every window-end representation is held to the bars (outputs and
-    dequantized states within 1e-3, codes equal in >= 99.9 % and at most one
-    step apart).  The quantized trajectory's distance from the unquantized fp32
-    one is reported beside the oracle's."""
-    wl = W_["gdn_tiny"]
-    H.log("free-running gdn_tiny")
+@pytest.mark.parametrize("name", ["gdn_tiny", "kda_free"])
+def test_free_running_tiny(name):
+    """A whole trajectory on the GPU alone: from the oracle's fp32 initial
+    state, its own quantization, the decode steps and the commits of its own
+    records, with nothing handed back from the oracle (GDN tiny: 256 steps, 16
+    commits; KDA: 8 tiles, 256 steps, 4 commits of 64 records, r = 8).  Every
+    output and every window-end representation is held to the bars (outputs
+    and dequantized states within 1e-3, codes equal in >= 99.9 % and at most
+    one step apart).  The quantized trajectory's distance from the unquantized
+    fp32 one is reported beside the oracle's."""
+    wl = W_["gdn_tiny"] if name == "gdn_tiny" else SMALL["kda_small"].with_(name="kda_free", steps=256)
+    H.log(f"free-running {wl.name}")
     cfg = H.ocfg(wl)
     S0 = H.oracle_prefill_state(wl)
     streams, tok = H.decode_tokens(wl)
