@@ -57,6 +57,9 @@ def parse():
     ap.add_argument("--gate-scale", type=float, default=0.1,
                     help="decay = exp(-s softplus(N(0,1))) for --long-trace (0.1: the workload's gates; "
                          "0.001: a long-memory variant)")
+    ap.add_argument("--commit-split", action="store_true",
+                    help="commit and quantize launch times on the KDA workload for r = 0, 4, 8 and 1, 2, 4 power "
+                         "sweeps, and the split of the commit into base, per-token and per-sweep costs; one JSON line")
     ap.add_argument("--profile-decode", action="store_true",
                     help="short run for profilers: setup, then the decode with rotating batches (the "
                          "roofline timing), eight steps of each dense baseline and one device copy for "
@@ -862,6 +865,44 @@ def sweep(args):
                           "speedup_vs_bf16": round(res["bf16"] / step, 3)}), flush=True)
 
 
+# ----------------------------------------------------------------------------- commit split
+
+def commit_split(args):
+    """Where the window commit's time goes (KDA workload, 8192 tiles, W = 64):
+    the commit and the quantization timed (per_launch_times) with r = 0, 4, 8
+    Compensator Tokens at 4 power sweeps and with 1 and 2 sweeps at r = 8, on
+    the same device-drawn state and tokens.  The commit at r = 0 is the base
+    (reconstruction of the window, smoothing, codes); the r = 8 times at 1, 2
+    and 4 sweeps give the cost of one token-sweep (least squares over the
+    three) and, with the base, the cost of a token outside its sweeps."""
+    from paper_2609_38166_amd import binding as B_, synth
+    wl0 = synth.WORKLOADS["kda_kimi"]
+    S0, toks = device_inputs(wl0, wl0.window, wl0.seed + 17)
+    rows = []
+    for r, pi in ((0, 4), (4, 4), (8, 1), (8, 2), (8, 4)):
+        wl = wl0.with_(n_comp=r, power_iters=pi)
+        dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=wl.window, n_comp=r, power_iters=pi,
+                            gate=wl.gate, code=wl.code)
+        kt = per_launch_times(wl, dims, S0, toks)
+        rows.append({"n_comp": r, "power_iters": pi, "commit_us": round(kt["commit_ms"] * 1e3, 1),
+                     "quantize_us": round(kt["quantize_ms"] * 1e3, 1)})
+        log(f"[commit split] {rows[-1]}")
+    base = rows[0]["commit_us"]
+    pis = np.array([1.0, 2.0, 4.0])
+    c8 = np.array([rows[2]["commit_us"], rows[3]["commit_us"], rows[4]["commit_us"]])
+    slope, icpt = np.polyfit(pis, c8, 1)
+    out = {"commit_split": {
+        "workload": "kda_kimi: 8192 tiles, W = 64, per-channel gate, int8",
+        "runs": rows,
+        "base_us": base,
+        "per_token_sweep_us": round(slope / 8, 2),
+        "per_token_outside_sweeps_us": round((icpt - base) / 8, 2),
+        "fp64_fma_bound_us_r8_4sweeps": round(8192 * 2.74e6 * 2 / 78.6e12 * 1e6, 1),
+        "note": ("base = the commit at r = 0 (window reconstruction, smoothing, codes); the r = 8 commit is "
+                 "base + 8 x (per-token cost + power_iters x per-token-sweep cost)")}}
+    print(json.dumps(out), flush=True)
+
+
 # ----------------------------------------------------------------------------- long trace
 
 def long_trace(args, every=1024, chunk=256):
@@ -939,6 +980,9 @@ def main():
         return
     if args.long_trace:
         long_trace(args)
+        return
+    if args.commit_split:
+        commit_split(args)
         return
     wl = synth.WORKLOADS[args.workload]
     dims = B_.make_dims(wl.batch, wl.heads_v, wl.heads_k, window=wl.window, n_comp=wl.n_comp,
