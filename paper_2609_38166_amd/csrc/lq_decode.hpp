@@ -598,8 +598,12 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
     // per-row scales, wave 0 (the BF16 state has unit scales and does not read them)
     if (!IsBF16<CODE>::value && tid < D / 4) dma16(a.scale + tvec + 4 * tid, lds_addr(sh.dlt));
     uint4 ck = make_uint4(0, 0, 0, 0), cu = make_uint4(0, 0, 0, 0);
-    if (ts < a.n_comp) {
-        const size_t cb = ((size_t)tile * a.n_comp + ts) * D + 8 * l16;
+    // Compensator Token j is read by slot 15 - j: a pass's records are dealt
+    // to the first slots, so at the early window positions the token readouts
+    // run on waves that walk no records, beside the walk instead of after it
+    const int cj = SLOTS - 1 - ts;
+    if (cj < a.n_comp) {
+        const size_t cb = ((size_t)tile * a.n_comp + cj) * D + 8 * l16;
         ck = *(const uint4 *)(a.comp_k + cb);
         cu = *(const uint4 *)(a.comp_u + cb);
     }
@@ -700,7 +704,13 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
                 }
             }
             carry = c;
-            if (lo == 0) base_vectors<CODE, KS>(sh, carry, kx, qx, cs, tid);   // carry = Gamma_{1:i}
+            if (lo == 0) {
+                // (opaque copies: nothing derived from them is hoisted out of
+                // the pass loop to be held across it)
+                float k2 = kx, q2 = qx, c2 = cs;
+                asm volatile("" : "+v"(k2), "+v"(q2), "+v"(c2));
+                base_vectors<CODE, KS>(sh, carry, k2, q2, c2, tid);   // carry = Gamma_{1:i}
+            }
         }
     };
     // the slot's records, newest first
@@ -815,8 +825,8 @@ __device__ __forceinline__ int decode_body(const DecodeArgs &a, DecodeShared<COD
         }
     }
 
-    // ---- Compensator Tokens: token ts, same decay as the base -------------------
-    if (ts < a.n_comp) {
+    // ---- Compensator Tokens: token cj, same decay as the base -------------------
+    if (cj < a.n_comp) {
         float kv[8], uv[8];
         unpack_h8(ck, kv);
         unpack_h8(cu, uv);
