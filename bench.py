@@ -750,15 +750,16 @@ def stream_read_ceiling(nbytes=4 << 30, reps=5):
     return {"gbps": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes}
 
 
-DECODE_SOURCES = ("lq_decode.hip", "lq_decode.hpp", "lq_device.hpp")
+DECODE_SOURCES = ("csrc/lq_decode.hip", "csrc/lq_decode.hpp", "csrc/lq_device.hpp", "build.py")
 
 
 def decode_source_sha():
-    """sha256 over the decode kernel's sources (launch, body, device helpers), in that order."""
+    """sha256 over the decode kernel's sources (launch, body, device helpers)
+    and the build script that sets its compiler options, in that order."""
     import hashlib
     h = hashlib.sha256()
     for f in DECODE_SOURCES:
-        h.update(open(os.path.join(ROOT, "paper_2609_38166_amd", "csrc", f), "rb").read())
+        h.update(open(os.path.join(ROOT, "paper_2609_38166_amd", f), "rb").read())
     return h.hexdigest()
 
 

@@ -2,6 +2,8 @@
 
 hipcc cross-compiles without a GPU.  Flags: -O3, IEEE fp32 division and square
 root (hipcc's default), denormals kept, packed-fp32 instructions disabled.
+Each source is compiled to an object of its own (with the scheduler options of
+SCHED below) and the objects are linked into the library.
 """
 from __future__ import annotations
 
@@ -9,6 +11,8 @@ import glob
 import os
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -18,11 +22,22 @@ BENCH_LIB = os.path.join(PKG, "libleapquant_bench.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-fno-gpu-flush-denormals-to-zero",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]
+
+# Machine scheduler options per source file (the LLVM AMDGPU backend's), each
+# measured against the default on the KDA workload (8192 tiles, W = 64, r = 8):
+#  - decode: the max-ILP strategy, 1.7% less time per launch over the window
+#    positions (2.2% on the GQA GDN layer), no spill;
+#  - tile kernel (quantize, commit): the AMDGPU register-pressure trackers,
+#    6% less time per commit (quantize within 2%).
+SCHED = {
+    "lq_decode.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "lq_tile.hip": ["-mllvm", "-amdgpu-use-amdgpu-trackers"],
+}
 
 
 def sources():
@@ -36,12 +51,22 @@ VALU_CP_LIB = os.path.join(PKG, "libleapquant_valucp.so")
 
 
 def _compile(srcs, out, verbose, defines=()):
-    tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, *defines, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
-           *srcs, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), file=sys.stderr)
-    subprocess.run(cmd, check=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc")]
+    with tempfile.TemporaryDirectory() as td:
+        def obj(src):
+            o = os.path.join(td, os.path.basename(src) + ".o")
+            cmd = [HIPCC, *FLAGS, *SCHED.get(os.path.basename(src), []), *defines, *inc, "-c", src, "-o", o]
+            if verbose:
+                print(" ".join(cmd), file=sys.stderr)
+            subprocess.run(cmd, check=True)
+            return o
+        with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+            objs = list(ex.map(obj, srcs))
+        tmp = out + ".tmp"
+        cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
+        if verbose:
+            print(" ".join(cmd), file=sys.stderr)
+        subprocess.run(cmd, check=True)
     os.replace(tmp, out)
 
 
