@@ -188,19 +188,22 @@ __device__ __forceinline__ double publish(TileShared &sh, double x, bool with_no
 // of its DPP row and return the 8 sums, times `scale`, in v.  The row's 16
 // lanes belong to one wave, so a row-private LDS region needs no workgroup
 // barrier: lane kb stores its partials at [b][kb] (rows of 17 words, so the
-// 8 channels a read touches sit in distinct banks, and consecutive rows start
-// 16 banks apart), lane kb then sums channel kb & 7 over the 16 lanes and
-// parks the sum in the row's spare word, which every lane reads back.
+// words a read touches sit in distinct banks, and consecutive rows start 16
+// banks apart); lane kb then sums channel kb & 7 over key blocks 8h .. 8h + 7
+// (h = kb >> 3), adds lane kb ^ 8's half by a row rotation, and lanes kb < 8
+// park the sums in the row's spare words, which every lane reads back.
 __device__ __forceinline__ void row_sum8(TileShared &sh, double *v, int kb, int vb, double scale) {
     double *r = sh.rowp[vb];
 #pragma unroll
     for (int b = 0; b < 8; ++b) r[17 * b + kb] = v[b];
     __builtin_amdgcn_wave_barrier();
-    const int c = kb & 7;
-    double t[4] = {r[17 * c], r[17 * c + 1], r[17 * c + 2], r[17 * c + 3]};
+    const int c = kb & 7, o = 17 * c + 8 * (kb >> 3);
+    double t[4] = {r[o], r[o + 1], r[o + 2], r[o + 3]};
 #pragma unroll
-    for (int l = 4; l < 16; ++l) t[l & 3] += r[17 * c + l];
-    if (kb < 8) r[17 * c + 16] = ((t[0] + t[1]) + (t[2] + t[3])) * scale;
+    for (int l = 4; l < 8; ++l) t[l & 3] += r[o + l];
+    double h = (t[0] + t[1]) + (t[2] + t[3]);
+    h += dpp<DPP_ROR8>(h);
+    if (kb < 8) r[17 * c + 16] = h * scale;
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int b = 0; b < 8; ++b) v[b] = r[17 * b + 16];
