@@ -462,15 +462,20 @@ __device__ __forceinline__ void tile_body(const TileArgs &A, TileShared &sh, int
         const double sc = ok ? ldexp(1.0, -ilogb(nrm * nrm)) : 0.0;
         for (int it = 0; ok && it < A.power_iters; ++it) {
             refresh();
+            // the eight reads of x issued together (one LDS round trip, not
+            // one per pair of channels)
+            double xv[8];
+#pragma unroll
+            for (int a = 0; a < 8; ++a) xv[a] = sh.vec[KP(kb, a)];
+            asm volatile("" : "+v"(xv[0]), "+v"(xv[1]), "+v"(xv[2]), "+v"(xv[3]), "+v"(xv[4]), "+v"(xv[5]),
+                         "+v"(xv[6]), "+v"(xv[7]));
             double y[VPT];
 #pragma unroll
-            for (int b = 0; b < VPT; ++b) y[b] = 0.0;
+            for (int b = 0; b < VPT; ++b) y[b] = m[0][b] * xv[0];
 #pragma unroll
-            for (int a = 0; a < 8; ++a) {
-                const double xa = sh.vec[KP(kb, a)];
+            for (int a = 1; a < 8; ++a)
 #pragma unroll
-                for (int b = 0; b < VPT; ++b) y[b] = fma(m[a][b], xa, y[b]);
-            }
+                for (int b = 0; b < VPT; ++b) y[b] = fma(m[a][b], xv[a], y[b]);
             row_sum8(sh, y, kb, vb, sc * xs);       // y_v = sc * sum_k M_kv (xs x_k)
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
