@@ -409,15 +409,18 @@ __device__ __forceinline__ void tile_body(const TileArgs &A, TileShared &sh, int
             // one record at a time, one key channel at a time, so only the
             // record's 8 values and one key are live beside the block
             const int nrec = hi - lo;
+            // this lane's parts of the staging addresses, held across the pass
+            refresh();
+            const float *vrow = &sh.val[0][VPT * vb];
+            const double *krow = &sh.key[0][kb];
 #pragma unroll 1
             for (int j = 0; j < nrec; ++j) {
-                refresh();
                 double u0[VPT];
 #pragma unroll
-                for (int b = 0; b < VPT; ++b) u0[b] = (double)sh.val[j][VPT * vb + b];
+                for (int b = 0; b < VPT; ++b) u0[b] = (double)vrow[j * D + b];
 #pragma unroll
                 for (int a = 0; a < 8; ++a) {
-                    const double k0 = sh.key[j][KP(kb, a)];
+                    const double k0 = krow[j * D + 16 * a];
 #pragma unroll
                     for (int b = 0; b < VPT; ++b) m[a][b] = fma(k0, u0[b], m[a][b]);
                 }
