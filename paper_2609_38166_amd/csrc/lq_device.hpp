@@ -49,11 +49,13 @@ __device__ __forceinline__ float row16_max(float x) {
     return x;
 }
 
+// (every lane of the row has a source under these controls, so the moves need
+// no old value: no register is cleared ahead of them)
 template <int CTRL>
 __device__ __forceinline__ double dpp(double x) {
     const int lo = __double2loint(x), hi = __double2hiint(x);
-    return __hiloint2double(__builtin_amdgcn_update_dpp(0, hi, CTRL, 0xF, 0xF, false),
-                            __builtin_amdgcn_update_dpp(0, lo, CTRL, 0xF, 0xF, false));
+    return __hiloint2double(__builtin_amdgcn_mov_dpp(hi, CTRL, 0xF, 0xF, true),
+                            __builtin_amdgcn_mov_dpp(lo, CTRL, 0xF, 0xF, true));
 }
 
 __device__ __forceinline__ double row16_sum(double x) {
