@@ -13,7 +13,8 @@
 //
 // Resources are those of the larger body: the commit holds a 128 x 128 fp64
 // tile in registers, so the kernel runs three workgroups per CU (the plain
-// decode runs four).
+// decode runs four); with the BF16 state, whose decode stages 32 KiB of state
+// per tile in LDS, two.
 #include "lq_decode.hpp"
 #include "lq_tile.hpp"
 
@@ -27,8 +28,10 @@ union FusedShared {
     TileShared t;
 };
 
+template <int CODE> struct FusedOcc { static constexpr int value = IsBF16<CODE>::value ? 2 : 3; };
+
 template <int GATE, int CODE, int RULE>
-__global__ __launch_bounds__(NT, 3) void decode_commit_kernel(DecodeArgs a, TileArgs c) {
+__global__ __launch_bounds__(NT, FusedOcc<CODE>::value) void decode_commit_kernel(DecodeArgs a, TileArgs c) {
     __shared__ FusedShared<CODE> sh;
     const int tile = blockIdx.x;
     const int n = decode_body<GATE, CODE, RULE>(a, sh.d, tile);
