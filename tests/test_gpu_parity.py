@@ -45,6 +45,10 @@ SMALL = {
     "w8_r16": W_["gdn_tiny"].with_(name="w8_r16", steps=64, window=8, n_comp=16),
     "w32_r4_nosmooth": W_["kda_kimi"].with_(name="w32_r4_nosmooth", batch=2, heads_v=4, heads_k=4,
                                             steps=64, window=32, n_comp=4, smooth=0, prefill=128),
+    # power-sweep counts other than the workloads' four: one sweep per token, and sixteen
+    "kda_pi1": W_["kda_kimi"].with_(name="kda_pi1", batch=2, heads_v=4, heads_k=4, steps=64, window=16,
+                                    n_comp=4, prefill=128, power_iters=1),
+    "gdn_pi16": W_["gdn_tiny"].with_(name="gdn_pi16", steps=64, window=16, n_comp=8, power_iters=16),
     # the largest window of the scalar gate (four record passes in the decode), and a
     # ragged tile count (3 requests x 5 heads)
     "gdn_w256": W_["gdn_tiny"].with_(name="gdn_w256", batch=2, heads_v=2, heads_k=2, steps=256, window=256,
@@ -189,6 +193,31 @@ def test_quantize_state_parity(code, r, smooth):
         assert cr["comp_rel"] <= 1e-3, cr
     assert not got["Z"][1].any() and not got["delta"][1].any()
     assert got["delta"][2][5] == 0 and got["delta"][2][99] == 0
+
+
+@pytest.mark.parametrize("power_iters", [1, 64])
+def test_quantize_state_parity_power_iters(power_iters):
+    """The sweep count at its ends (one sweep per token, and the 64 the ABI
+    allows): codes, scales and Compensator Tokens as the oracle's."""
+    H.log(f"quantize power_iters={power_iters}")
+    wl = W_["gdn_tiny"].with_(batch=4, heads_v=8, heads_k=8, n_comp=8, power_iters=power_iters)
+    S = _states_with_edges(wl.tiles, 300 + power_iters)
+    cfg = H.ocfg(wl)
+    exp = {"Z": [], "delta": [], "c": [], "Kt": [], "Ut": []}
+    for i in range(wl.tiles):
+        rep = O.quantize(cfg, S[i])
+        for k_ in exp:
+            exp[k_].append(getattr(rep, k_))
+    exp = {k_: np.stack(v_) for k_, v_ in exp.items()}
+    dims = H.gdims(wl)
+    st = B.State.empty(dims)
+    B.leapquant_quantize_state(dims, H.dev(S.transpose(0, 2, 1).astype(np.float32)), st)
+    got = H.download_rep(st)
+    cr = H.compare_rep(cfg, got, exp, wl.code)
+    H.log(cr)
+    assert cr["code_eq"] >= 0.999 and cr["code_maxdiff"] <= 1, cr
+    assert cr["deq_rel"] <= 1e-3 and cr["delta_rel"] <= 1e-5 and cr["c_rel"] <= 1e-5, cr
+    assert cr["comp_rel"] <= 1e-3, cr
 
 
 def test_quantize_state_parity_bf16():
