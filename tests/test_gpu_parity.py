@@ -60,6 +60,9 @@ SMALL = {
     "kda_w256": W_["kda_kimi"].with_(name="kda_w256", batch=1, heads_v=2, heads_k=2, steps=256, window=256,
                                      prefill=128),
     "ragged_3x5": W_["gdn_tiny"].with_(name="ragged_3x5", batch=3, heads_v=5, heads_k=5, steps=48, prefill=128),
+    # a launch of one workgroup
+    "kda_one_tile": W_["kda_kimi"].with_(name="kda_one_tile", batch=1, heads_v=1, heads_k=1, steps=80, window=32,
+                                         prefill=128),
     # b_t = 0 rows of the instance table: Mamba2 (scalar decay), GLA / RWKV6 (per-channel)
     "mamba2_small": W_["gdn_tiny"].with_(name="mamba2_small", rule=1),
     "gla_small": W_["kda_kimi"].with_(name="gla_small", batch=2, heads_v=4, heads_k=4, steps=128,
